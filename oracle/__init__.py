@@ -1,0 +1,150 @@
+"""fp64 CPU oracle for paged rollout attention (TEST INFRASTRUCTURE).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package. It shares no code with the HIP library
+(`paper_2603_18815_amd`) and never imports it.
+
+The arithmetic lives in `attn_oracle.c` (plain loops, fp64, libm exp/log); this
+module only marshals numpy arrays into it. What each function computes and the
+readings it adopts where the paper is silent are stated at the top of that file.
+Every function here is pinned by the `-m "not gpu"` tests in
+`tests/test_oracle_pins.py` (library routine, closed forms, invariants, brute
+force, hand-derived fixtures under `tests/golden/`).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+
+_u16p = np.ctypeslib.ndpointer(dtype=np.uint16, flags="C_CONTIGUOUS")
+_i32p = np.ctypeslib.ndpointer(dtype=np.int32, flags="C_CONTIGUOUS")
+_f64p = np.ctypeslib.ndpointer(dtype=np.float64, flags="C_CONTIGUOUS")
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_build.LIB) or (
+        os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC)
+    ):
+        _build.build()
+    lib = ctypes.CDLL(_build.LIB)
+    c_i64, c_int, c_dbl = ctypes.c_int64, ctypes.c_int, ctypes.c_double
+    lib.oracle_decode_f64.argtypes = [_u16p, _u16p, _u16p, _i32p, c_i64, _i32p, c_int, c_int,
+                                      c_int, c_int, c_int, c_dbl, _f64p, _f64p]
+    lib.oracle_decode_f64.restype = c_int
+    lib.oracle_append_f64.argtypes = [_u16p, _i32p, _i32p, _u16p, _u16p, _i32p, c_i64, c_int,
+                                      c_int, c_int, c_int, c_int, c_dbl, _f64p, _f64p]
+    lib.oracle_append_f64.restype = c_int
+    lib.oracle_page_write.argtypes = [_u16p, _u16p, _i32p, _i32p, _i32p, c_i64, c_int, c_int,
+                                      c_int, c_int, _u16p, _u16p]
+    lib.oracle_page_write.restype = c_int
+    lib.oracle_page_gather.argtypes = [_u16p, _u16p, _i32p, c_i64, _i32p, _i32p, c_int, c_int,
+                                       c_int, c_int, _u16p, _u16p]
+    lib.oracle_page_gather.restype = c_int
+    _lib = lib
+    return lib
+
+
+def _u16(a):
+    a = np.asarray(a)
+    if a.dtype != np.uint16:
+        raise TypeError("bf16 data must be passed as uint16 bit patterns")
+    return np.ascontiguousarray(a)
+
+
+def _i32(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def pool_dims(k_pool, v_pool, page_size, head_dim):
+    """(num_pages, Hkv) of a pool pair; K is [pages][Hkv][P][D], V is [pages][Hkv][D][P]."""
+    if k_pool.ndim != 4 or v_pool.ndim != 4:
+        raise ValueError("pools must be 4-D")
+    n, hkv, p, d = k_pool.shape
+    if (p, d) != (page_size, head_dim) or v_pool.shape != (n, hkv, head_dim, page_size):
+        raise ValueError(f"pool shapes {k_pool.shape} / {v_pool.shape} do not match the layout")
+    return n, hkv
+
+
+def decode(q, k_pool, v_pool, block_table, kv_lens, scale):
+    """Decode attention, fp64. q bf16 bits [B][Hq][D]; returns (out [B][Hq][D], lse [B][Hq])."""
+    lib = _load()
+    q = _u16(q)
+    k_pool, v_pool = _u16(k_pool), _u16(v_pool)
+    B, Hq, D = q.shape
+    P = k_pool.shape[2]
+    _, Hkv = pool_dims(k_pool, v_pool, P, D)
+    bt = _i32(block_table)
+    lens = _i32(kv_lens)
+    out = np.zeros((B, Hq, D), np.float64)
+    lse = np.zeros((B, Hq), np.float64)
+    rc = lib.oracle_decode_f64(q, k_pool, v_pool, bt, bt.shape[1] if bt.ndim == 2 else 0, lens,
+                               B, Hq, Hkv, P, D, float(scale), out, lse)
+    if rc != 0:
+        raise RuntimeError(f"oracle_decode_f64 failed ({rc})")
+    return out, lse
+
+
+def append(q, cu_q, ctx_lens, k_pool, v_pool, block_table, scale):
+    """Append attention, fp64. q bf16 bits [total_q][Hq][D]; returns (out, lse)."""
+    lib = _load()
+    q = _u16(q)
+    k_pool, v_pool = _u16(k_pool), _u16(v_pool)
+    total_q, Hq, D = q.shape
+    P = k_pool.shape[2]
+    _, Hkv = pool_dims(k_pool, v_pool, P, D)
+    cu = _i32(cu_q)
+    ctx = _i32(ctx_lens)
+    B = ctx.shape[0]
+    if cu.shape[0] != B + 1 or cu[-1] != total_q:
+        raise ValueError("cu_q must have B+1 entries ending at total_q")
+    bt = _i32(block_table)
+    out = np.zeros((total_q, Hq, D), np.float64)
+    lse = np.zeros((total_q, Hq), np.float64)
+    rc = lib.oracle_append_f64(q, cu, ctx, k_pool, v_pool, bt, bt.shape[1] if bt.ndim == 2 else 0,
+                               B, Hq, Hkv, P, D, float(scale), out, lse)
+    if rc != 0:
+        raise RuntimeError(f"oracle_append_f64 failed ({rc})")
+    return out, lse
+
+
+def page_write(k_new, v_new, cu_new, start_pos, block_table, k_pool, v_pool):
+    """Return copies of (k_pool, v_pool) with the new tokens scattered in (bit copy)."""
+    lib = _load()
+    k_new, v_new = _u16(k_new), _u16(v_new)
+    kp, vp = _u16(k_pool).copy(), _u16(v_pool).copy()
+    P, D = kp.shape[2], kp.shape[3]
+    _, Hkv = pool_dims(kp, vp, P, D)
+    cu = _i32(cu_new)
+    sp = _i32(start_pos)
+    bt = _i32(block_table)
+    rc = lib.oracle_page_write(k_new, v_new, cu, sp, bt, bt.shape[1], sp.shape[0], Hkv, P, D,
+                               kp, vp)
+    if rc != 0:
+        raise RuntimeError(f"oracle_page_write failed ({rc})")
+    return kp, vp
+
+
+def page_gather(k_pool, v_pool, block_table, lens, cu_out):
+    """Logical tokens [0, lens[b]) of every row, packed token-major: (k [total][Hkv][D], v)."""
+    lib = _load()
+    kp, vp = _u16(k_pool), _u16(v_pool)
+    P, D = kp.shape[2], kp.shape[3]
+    _, Hkv = pool_dims(kp, vp, P, D)
+    lens = _i32(lens)
+    cu = _i32(cu_out)
+    bt = _i32(block_table)
+    total = int(cu[-1]) if cu.size else 0
+    k_out = np.zeros((total, Hkv, D), np.uint16)
+    v_out = np.zeros((total, Hkv, D), np.uint16)
+    rc = lib.oracle_page_gather(kp, vp, bt, bt.shape[1], lens, cu, lens.shape[0], Hkv, P, D,
+                                k_out, v_out)
+    if rc != 0:
+        raise RuntimeError(f"oracle_page_gather failed ({rc})")
+    return k_out, v_out

@@ -1,0 +1,245 @@
+/*
+ * fp64 CPU oracle for paged rollout attention.
+ *
+ * TEST INFRASTRUCTURE. Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg may call anything in this directory. It shares no code,
+ * header, table or helper with the HIP library; it reads the same plain arrays.
+ *
+ * What it computes. The ProRL Agent paper (arXiv 2603.18815) runs every agent
+ * step as one LLM completion over the whole conversation so far (Sec. 3.3.2),
+ * routes all calls of a task to one backend so the cached prefix is reused
+ * (Sec. 3.3.2, load balancing), and keeps earlier turns' token ids while only
+ * new observations are tokenised and appended (Sec. 3.3.3). On the GPU this is
+ * attention of new tokens against a per-trajectory cache of keys and values.
+ * The paper gives no attention formula, so the oracle is the textbook
+ * definition of scaled dot-product attention with grouped KV heads, written
+ * out in fp64:
+ *
+ *   s_j  = scale * sum_d q[d] * k_j[d]
+ *   m    = max_j s_j
+ *   w_j  = exp(s_j - m),      Z = sum_j w_j
+ *   out  = (sum_j w_j * v_j) / Z,  lse = m + ln Z
+ *
+ * Readings the paper leaves open (each is also listed in the design notes):
+ *   - query head h reads KV head g = h / G with G = Hq / Hkv (contiguous groups);
+ *   - a decode row attends its kv_len cached keys, the current token included;
+ *   - append query i of a row sits at absolute position ctx + i and attends keys
+ *     0 .. ctx + i inclusive (bottom-right causal alignment);
+ *   - an empty key set gives out = 0 and lse = -inf;
+ *   - bf16 inputs are widened exactly (bits << 16 -> fp32 -> fp64).
+ *
+ * Paged layout (the address formula the library's header defines), with P the
+ * page size and D the head dimension; logical token j of row b lives in
+ * physical page bt[b * bt_stride + j / P] at slot j % P:
+ *   K element (page, g, slot, d) at (((page * Hkv + g) * P + slot) * D + d)
+ *   V element (page, g, slot, d) at (((page * Hkv + g) * D + d) * P + slot)
+ * i.e. K pages are token-major and V pages are dimension-major.
+ *
+ * P and D are parameters here (the GPU library fixes P = 16, D = 128) so that
+ * tiny hand-checkable cases can be run.
+ *
+ * Build: gcc -O2 -fopenmp -shared -fPIC (no -ffast-math), see oracle/build.py.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+static double bf16_to_f64(uint16_t bits) {
+  uint32_t u = (uint32_t)bits << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+static size_t k_index(int64_t page, int g, int slot, int d, int Hkv, int P, int D) {
+  return (((size_t)page * Hkv + g) * P + slot) * D + d;
+}
+
+static size_t v_index(int64_t page, int g, int slot, int d, int Hkv, int P, int D) {
+  return (((size_t)page * Hkv + g) * D + d) * P + slot;
+}
+
+/* Physical page holding logical token j of row b. */
+static int64_t page_of(const int32_t *bt, int64_t bt_stride, int b, int64_t j, int P) {
+  return bt[(int64_t)b * bt_stride + j / P];
+}
+
+/*
+ * Attention of one query vector q[0..D) (bf16 bits) over the first nkeys
+ * logical tokens of row b, KV head g. Writes out[0..D) and *lse.
+ * scores: caller scratch of at least nkeys doubles.
+ */
+static void attend_one(const uint16_t *q, const uint16_t *k_pool, const uint16_t *v_pool,
+                       const int32_t *bt, int64_t bt_stride, int b, int g, int64_t nkeys,
+                       int Hkv, int P, int D, double scale, double *scores, double *out,
+                       double *lse) {
+  for (int d = 0; d < D; ++d) out[d] = 0.0;
+  if (nkeys <= 0) {
+    *lse = -INFINITY;
+    return;
+  }
+  double m = -INFINITY;
+  for (int64_t j = 0; j < nkeys; ++j) {
+    int64_t page = page_of(bt, bt_stride, b, j, P);
+    int slot = (int)(j % P);
+    double dot = 0.0;
+    for (int d = 0; d < D; ++d)
+      dot += bf16_to_f64(q[d]) * bf16_to_f64(k_pool[k_index(page, g, slot, d, Hkv, P, D)]);
+    scores[j] = scale * dot;
+    if (scores[j] > m) m = scores[j];
+  }
+  double z = 0.0;
+  for (int64_t j = 0; j < nkeys; ++j) {
+    int64_t page = page_of(bt, bt_stride, b, j, P);
+    int slot = (int)(j % P);
+    double w = exp(scores[j] - m);
+    z += w;
+    for (int d = 0; d < D; ++d)
+      out[d] += w * bf16_to_f64(v_pool[v_index(page, g, slot, d, Hkv, P, D)]);
+  }
+  for (int d = 0; d < D; ++d) out[d] /= z;
+  *lse = m + log(z);
+}
+
+/*
+ * Decode: one query token per row.
+ *   q        bf16 [B][Hq][D]
+ *   kv_lens  [B]   keys attended by each row (current token included)
+ *   out      f64 [B][Hq][D],  lse f64 [B][Hq] (may be NULL)
+ * Returns 0, or -1 on bad shape arguments.
+ */
+int oracle_decode_f64(const uint16_t *q, const uint16_t *k_pool, const uint16_t *v_pool,
+                      const int32_t *block_table, int64_t bt_stride, const int32_t *kv_lens,
+                      int B, int Hq, int Hkv, int P, int D, double scale, double *out,
+                      double *lse) {
+  if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || P <= 0 || D <= 0) return -1;
+  const int G = Hq / Hkv;
+  int64_t max_len = 0;
+  for (int b = 0; b < B; ++b)
+    if (kv_lens[b] > max_len) max_len = kv_lens[b];
+  int failed = 0;
+#pragma omp parallel
+  {
+    double *scores = (double *)malloc(sizeof(double) * (size_t)(max_len > 0 ? max_len : 1));
+    if (!scores) {
+#pragma omp atomic write
+      failed = 1;
+    }
+#pragma omp for collapse(2) schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) {
+      for (int h = 0; h < Hq; ++h) {
+        if (!scores) continue;
+        double lse_bh;
+        attend_one(q + ((size_t)b * Hq + h) * D, k_pool, v_pool, block_table, bt_stride, b,
+                   h / G, kv_lens[b], Hkv, P, D, scale, scores, out + ((size_t)b * Hq + h) * D,
+                   &lse_bh);
+        if (lse) lse[(size_t)b * Hq + h] = lse_bh;
+      }
+    }
+    free(scores);
+  }
+  return failed ? -2 : 0;
+}
+
+/*
+ * Append (chunked causal prefill against the cache). Row b owns queries
+ * cu_q[b] .. cu_q[b+1]-1; query i of the row (i from 0) attends logical keys
+ * 0 .. ctx_lens[b] + i. The chunk's own keys and values are already in the pool
+ * at positions ctx_lens[b] .. ctx_lens[b] + T_b - 1.
+ *   q    bf16 [total_q][Hq][D]
+ *   out  f64 [total_q][Hq][D], lse f64 [total_q][Hq] (may be NULL)
+ */
+int oracle_append_f64(const uint16_t *q, const int32_t *cu_q, const int32_t *ctx_lens,
+                      const uint16_t *k_pool, const uint16_t *v_pool, const int32_t *block_table,
+                      int64_t bt_stride, int B, int Hq, int Hkv, int P, int D, double scale,
+                      double *out, double *lse) {
+  if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || P <= 0 || D <= 0) return -1;
+  const int G = Hq / Hkv;
+  int64_t total_q = B > 0 ? cu_q[B] : 0;
+  int64_t max_keys = 1;
+  for (int b = 0; b < B; ++b) {
+    int64_t n = (int64_t)ctx_lens[b] + (cu_q[b + 1] - cu_q[b]);
+    if (n > max_keys) max_keys = n;
+  }
+  int failed = 0;
+#pragma omp parallel
+  {
+    double *scores = (double *)malloc(sizeof(double) * (size_t)max_keys);
+    if (!scores) {
+#pragma omp atomic write
+      failed = 1;
+    }
+#pragma omp for collapse(2) schedule(dynamic, 1)
+    for (int64_t t = 0; t < total_q; ++t) {
+      for (int h = 0; h < Hq; ++h) {
+        if (!scores) continue;
+        int b = 0; /* row that owns packed query t */
+        while (b + 1 <= B && cu_q[b + 1] <= t) ++b;
+        int64_t i = t - cu_q[b];
+        int64_t nkeys = (int64_t)ctx_lens[b] + i + 1;
+        double lse_th;
+        attend_one(q + ((size_t)t * Hq + h) * D, k_pool, v_pool, block_table, bt_stride, b,
+                   h / G, nkeys, Hkv, P, D, scale, scores, out + ((size_t)t * Hq + h) * D,
+                   &lse_th);
+        if (lse) lse[(size_t)t * Hq + h] = lse_th;
+      }
+    }
+    free(scores);
+  }
+  return failed ? -2 : 0;
+}
+
+/*
+ * Page write: for each row b and new token t of that row, logical position
+ * pos = start_pos[b] + t receives k_new / v_new row cu_new[b] + t for every KV
+ * head. A bit copy; no other pool element changes.
+ *   k_new, v_new  bf16 [total_new][Hkv][D]
+ */
+int oracle_page_write(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
+                      const int32_t *start_pos, const int32_t *block_table, int64_t bt_stride,
+                      int B, int Hkv, int P, int D, uint16_t *k_pool, uint16_t *v_pool) {
+  if (B < 0 || Hkv <= 0 || P <= 0 || D <= 0) return -1;
+  for (int b = 0; b < B; ++b) {
+    for (int64_t t = 0; t < (int64_t)cu_new[b + 1] - cu_new[b]; ++t) {
+      int64_t pos = (int64_t)start_pos[b] + t;
+      int64_t page = page_of(block_table, bt_stride, b, pos, P);
+      int slot = (int)(pos % P);
+      size_t src_tok = (size_t)cu_new[b] + (size_t)t;
+      for (int g = 0; g < Hkv; ++g) {
+        for (int d = 0; d < D; ++d) {
+          size_t src = (src_tok * Hkv + g) * D + d;
+          k_pool[k_index(page, g, slot, d, Hkv, P, D)] = k_new[src];
+          v_pool[v_index(page, g, slot, d, Hkv, P, D)] = v_new[src];
+        }
+      }
+    }
+  }
+  return 0;
+}
+
+/*
+ * Gather: logical tokens 0 .. lens[b]-1 of every row, copied out of the pages
+ * into packed token-major arrays k_out, v_out bf16 [total][Hkv][D], row b
+ * starting at cu_out[b].
+ */
+int oracle_page_gather(const uint16_t *k_pool, const uint16_t *v_pool, const int32_t *block_table,
+                       int64_t bt_stride, const int32_t *lens, const int32_t *cu_out, int B,
+                       int Hkv, int P, int D, uint16_t *k_out, uint16_t *v_out) {
+  if (B < 0 || Hkv <= 0 || P <= 0 || D <= 0) return -1;
+  for (int b = 0; b < B; ++b) {
+    for (int64_t j = 0; j < lens[b]; ++j) {
+      int64_t page = page_of(block_table, bt_stride, b, j, P);
+      int slot = (int)(j % P);
+      size_t dst_tok = (size_t)cu_out[b] + (size_t)j;
+      for (int g = 0; g < Hkv; ++g) {
+        for (int d = 0; d < D; ++d) {
+          size_t dst = (dst_tok * Hkv + g) * D + d;
+          k_out[dst] = k_pool[k_index(page, g, slot, d, Hkv, P, D)];
+          v_out[dst] = v_pool[v_index(page, g, slot, d, Hkv, P, D)];
+        }
+      }
+    }
+  }
+  return 0;
+}
