@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Benchmark of one rollout-attention step on one MI355X.
+
+A step is one pass of the whole hot path over one batch of seeded synthetic
+input at the Qwen3-8B GQA shape (Hq = 32, Hkv = 8, head dim 128, 16-token
+pages, bf16 K/V, fp32 outputs):
+  1. kv_page_write  - the step's new tokens: one decode token per decode row
+                      and every append row's observation chunk;
+  2. rollout_attn_decode - B = 64 trajectories, context uniform in
+                      [4096, 32768] keys, shuffled pages (split + combine kernels);
+  3. rollout_attn_append - B = 32 trajectories, cached context uniform in
+                      [2048, 24576], chunk uniform in [64, 2048] tokens.
+Inputs are resident in HBM before timing starts. Each call is bracketed by HIP
+events on the stream the library launches on (torch's current stream).
+
+Printed: one JSON line. `value` is the decode attention's algorithmic HBM
+GB/s (K/V bytes of every attended key + q + out + block table + lengths,
+divided by the decode call's time); the append's algorithmic TFLOP/s (only
+unmasked query-key pairs, two matrix products each) is reported beside it.
+`roofline` is the decode kernel pair against the 8 TB/s HBM peak,
+`roofline_append` the append kernel against the 2.5 PFLOP/s dense bf16 peak.
+`cpu_baseline` is the fp64 CPU oracle on a bounded sample of the same inputs.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+SCALE = 1.0 / math.sqrt(128)
+
+
+def decode_bytes(w) -> int:
+    L = w.kv_lens.astype(np.int64)
+    D = w.head_dim
+    per_row = (L * w.Hkv * D * 2 * 2 + w.Hq * D * 2 + w.Hq * D * 4
+               + 4 * ((L + w.page_size - 1) // w.page_size) + 4)
+    return int(per_row.sum())
+
+
+def append_flops(w) -> int:
+    T = w.q_lens.astype(np.int64)
+    C = w.ctx_lens.astype(np.int64)
+    return int(4 * w.head_dim * w.Hq * (T * C + T * (T + 1) // 2).sum())
+
+
+def write_bytes(n_new: int, Hkv: int, D: int = 128) -> int:
+    return 2 * n_new * Hkv * D * 2 * 2
+
+
+def cpu_baseline(wd, td, wa, ta, seconds: float):
+    """Time the fp64 oracle on bounded samples of the benchmark's own inputs."""
+    import oracle
+    import torch
+    from synth import bits, compact_rows
+
+    cores = oracle.num_threads()
+    # decode: whole rows of the decode workload, taken in a fixed order until the budget
+    rng = np.random.default_rng(0)
+    order = rng.permutation(wd.kv_lens.shape[0])
+    dev = td.k_pool.device
+    done_bytes, spent, rows_done = 0, 0.0, 0
+    table = wd.decode_table()
+    for chunk in np.array_split(order, 8):
+        k, v, bt = compact_rows(td.k_pool, td.v_pool, table[chunk], wd.kv_lens[chunk])
+        q = bits(td.q_decode[torch.as_tensor(chunk, device=dev)])
+        t0 = time.perf_counter()
+        oracle.decode(q, k, v, bt, wd.kv_lens[chunk], SCALE)
+        spent += time.perf_counter() - t0
+        sub = wd.kv_lens[chunk].astype(np.int64)
+        done_bytes += int((sub * wd.Hkv * 128 * 4 + wd.Hq * 128 * 6
+                           + 4 * ((sub + 15) // 16) + 4).sum())
+        rows_done += len(chunk)
+        if spent > seconds:
+            break
+    dec = {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
+           "sample": f"decode, {rows_done} of {wd.kv_lens.shape[0]} rows of the decode "
+                     f"workload (all heads), {spent:.1f} s wall"}
+    # append: single queries (query i of a row == a one-token chunk at ctx + i)
+    cu = wa.cu_q()
+    qs, ctx1, rows = [], [], []
+    for r in rng.permutation(wa.q_lens.shape[0])[:4]:
+        for i in rng.integers(0, int(wa.q_lens[r]), 8):
+            qs.append(int(cu[r]) + int(i))
+            ctx1.append(int(wa.ctx_lens[r]) + int(i))
+            rows.append(int(r))
+    ctx1 = np.array(ctx1, np.int32)
+    k, v, bt = compact_rows(ta.k_pool, ta.v_pool, wa.append_table()[np.array(rows)], ctx1 + 1)
+    q = bits(ta.q_append[torch.as_tensor(qs, device=dev)])
+    t0 = time.perf_counter()
+    oracle.append(q, np.arange(len(qs) + 1, dtype=np.int32), ctx1, k, v, bt, SCALE)
+    spent_a = time.perf_counter() - t0
+    flops = 4 * 128 * wa.Hq * int((ctx1.astype(np.int64) + 1).sum())
+    app = {"value": flops / spent_a / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+           "sample": f"append, {len(qs)} single queries (all heads) from 4 rows of the append "
+                     f"workload, {spent_a:.2f} s wall"}
+    return dec, app
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="budget of the decode leg of the CPU oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(rows shard by trajectory with no exchange; see the design notes).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2603_18815_amd as ra
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wd, wa = synth.config(2), synth.config(3)
+    td, ta = synth.make_tensors(wd, dev), synth.make_tensors(wa, dev)
+
+    def i32(x):
+        return torch.as_tensor(np.ascontiguousarray(np.asarray(x, np.int32)), device=dev)
+
+    # decode workload: the decode token of each row is written at kv_len - 1
+    bt_d, cu_d, st_d = synth.write_plan(wd)
+    bt_a, cu_a, st_a = synth.write_plan(wa)
+    kv_d = ra.PagedKV(td.k_pool, td.v_pool, i32(wd.decode_table()))
+    kv_a = ra.PagedKV(ta.k_pool, ta.v_pool, i32(wa.append_table()))
+    kv_dw = kv_d.with_table(i32(bt_d))
+    kv_aw = kv_a.with_table(i32(bt_a))
+    cu_d_t, st_d_t, cu_a_t, st_a_t = i32(cu_d), i32(st_d), i32(cu_a), i32(st_a)
+    kv_lens = i32(wd.kv_lens)
+    cu_q, ctx = i32(wa.cu_q()), i32(wa.ctx_lens)
+    max_kv_d = int(wd.kv_lens.max())
+    max_q, max_kv_a = int(wa.q_lens.max()), int((wa.ctx_lens + wa.q_lens).max())
+    out_d = torch.empty((wd.kv_lens.shape[0], wd.Hq, 128), dtype=torch.float32, device=dev)
+    out_a = torch.empty((int(wa.q_lens.sum()), wa.Hq, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty(ra.decode_workspace_size(wd.kv_lens.shape[0], wd.Hq, wd.Hkv, max_kv_d),
+                     dtype=torch.uint8, device=dev)
+    max_new_d, max_pos_d = 1, max_kv_d
+    max_new_a, max_pos_a = max_q, max_kv_a
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        ra.kv_page_write(td.k_new, td.v_new, cu_d_t, st_d_t, kv_dw, max_new_d, max_pos_d)
+        ra.kv_page_write(ta.k_new, ta.v_new, cu_a_t, st_a_t, kv_aw, max_new_a, max_pos_a)
+        if ev is not None:
+            ev[1].record()
+        ra.decode(td.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
+        if ev is not None:
+            ev[2].record()
+        ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    w_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
+    d_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
+    a_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+    step_ms = np.array([e[0].elapsed_time(e[3]) for e in events])
+
+    dbytes = decode_bytes(wd)
+    aflops = append_flops(wa)
+    n_new = int(cu_d[-1] + cu_a[-1])
+    wbytes = write_bytes(n_new, wd.Hkv)
+    dec_gbs = dbytes / (d_ms.mean() * 1e-3) / 1e9
+    app_tfs = aflops / (a_ms.mean() * 1e-3) / 1e12
+
+    cpu_dec = cpu_app = None
+    if not args.no_cpu_baseline:
+        cpu_dec, cpu_app = cpu_baseline(wd, td, wa, ta, args.cpu_seconds)
+
+    rec = {
+        "metric": "decode attn HBM GB/s (% of peak) + append TFLOP/s, Qwen3-8B GQA shape",
+        "value": round(dec_gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(float(step_ms.mean()), 4),
+        "wall_ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; bf16 N(0,1) K/V/q, shuffled 16-token pages)",
+        "config": {
+            "workload": "rollout attention step, Qwen3-8B GQA (Hq=32, Hkv=8, d=128, page 16): "
+                        "page write + decode B=64 L~U[4096,32768] + append B=32 "
+                        "ctx~U[2048,24576] T~U[64,2048]",
+            "decode_rows": int(wd.kv_lens.shape[0]),
+            "decode_kv_tokens": int(wd.kv_lens.sum()),
+            "append_rows": int(wa.q_lens.shape[0]),
+            "append_q_tokens": int(wa.q_lens.sum()),
+            "append_ctx_tokens": int(wa.ctx_lens.sum()),
+            "new_tokens_written": n_new,
+            "parallelism": "1 GPU",
+        },
+        "decode": {"ms": round(float(d_ms.mean()), 4), "ms_min": round(float(d_ms.min()), 4),
+                   "algorithmic_bytes": dbytes, "GB_s": round(dec_gbs, 1),
+                   "frac_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
+        "append": {"ms": round(float(a_ms.mean()), 4), "ms_min": round(float(a_ms.min()), 4),
+                   "algorithmic_flops": aflops, "TFLOP_s": round(app_tfs, 1),
+                   "frac_bf16_peak": round(app_tfs / BF16_PEAK_TFLOPS, 4)},
+        "page_write": {"ms": round(float(w_ms.mean()), 4), "algorithmic_bytes": wbytes,
+                       "GB_s": round(wbytes / (w_ms.mean() * 1e-3) / 1e9, 1)},
+        "roofline": {"kernel": "rollout_attn_decode (decode_split_kernel + decode_combine_kernel)",
+                     "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "roofline_append": {"kernel": "append_kernel", "bound": "mfma",
+                            "achieved": round(app_tfs, 1), "peak": BF16_PEAK_TFLOPS,
+                            "unit": "TFLOP/s", "frac": round(app_tfs / BF16_PEAK_TFLOPS, 4),
+                            "traffic": None},
+        "cpu_baseline": cpu_dec,
+        "cpu_baseline_append": cpu_app,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

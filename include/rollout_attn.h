@@ -1,0 +1,184 @@
+/*
+ * rollout_attn.h — C ABI of the MI355X (gfx950) rollout-attention library.
+ *
+ * The library implements the GPU work that dominates multi-turn agent rollouts
+ * as described in "ProRL Agent: Rollout-as-a-Service for RL Training of
+ * Multi-Turn LLM Agents" (arXiv 2603.18815):
+ *   - every agent step is one LLM completion over the whole conversation
+ *     history (Sec. 3.3.2), i.e. a decode step of one new token per trajectory
+ *     against that trajectory's cached keys and values;
+ *   - all calls of one task go to one backend so that its cached prefix is
+ *     reused (Sec. 3.3.2, load balancing), so each trajectory keeps a
+ *     persistent paged KV cache across turns;
+ *   - earlier turns keep their token ids and only new observations are
+ *     tokenised and appended (Sec. 3.3.3), i.e. a causal chunked prefill of the
+ *     observation tokens against the existing cache ("append").
+ * The paper states no attention formula; the library computes standard
+ * scaled dot-product softmax attention with grouped KV heads (query head h
+ * reads KV head h / (Hq / Hkv)), bf16 inputs, fp32 accumulation and fp32
+ * outputs.
+ *
+ * Conventions for every entry point
+ *   - All array arguments are DEVICE pointers unless marked "host". The caller
+ *     owns every buffer (pools, tables, outputs, workspace); the library
+ *     allocates nothing and keeps no pointer after it returns.
+ *   - Work is enqueued asynchronously on `stream` (0 = the null stream). Buffers
+ *     must stay alive until the stream has executed the enqueued kernels.
+ *     Concurrent calls on different streams are safe if their outputs and
+ *     workspaces do not overlap.
+ *   - Every function returns an ra_status. Arguments the host can check are
+ *     checked before any HIP call. Nothing aborts.
+ *   - Zero work (B == 0, total_q == 0, total_new == 0) returns RA_OK without
+ *     launching anything.
+ *   - Device-resident metadata (lengths, block tables, cu_* offsets) is a
+ *     precondition and is not read by the host: lengths >= 0, every position
+ *     used lies below bt_stride * page_size, page ids lie in [0, num_pages),
+ *     cu_* arrays are non-decreasing with cu[0] = 0. As a guard against
+ *     memory faults the kernels clamp page ids into [0, num_pages) and
+ *     lengths to the host-provided maxima; violating inputs give undefined
+ *     numbers, never an out-of-bounds access.
+ *   - Results are deterministic: the same inputs give bitwise the same
+ *     outputs, independent of which physical pages the block table names.
+ *
+ * Paged KV layout (ABI version 1). Page size P = 16 tokens, head dim D = 128.
+ * Logical token j of row b lives in physical page bt[b * bt_stride + j / P]
+ * at slot j % P. Within a page each KV head owns one contiguous 4 KiB block:
+ *   K pool  bf16 [num_pages][Hkv][P][D]   element (page, g, slot, d) at
+ *           ((page * Hkv + g) * P + slot) * D + d           (token-major)
+ *   V pool  bf16 [num_pages][Hkv][D][P]   element (page, g, slot, d) at
+ *           ((page * Hkv + g) * D + d) * P + slot           (dim-major)
+ * V is stored dimension-major so that the matrix-core operand for P·V (keys
+ * along the contraction dimension) is a contiguous 16-byte read.
+ */
+#ifndef ROLLOUT_ATTN_H
+#define ROLLOUT_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RA_ABI_VERSION 1
+#define RA_PAGE_SIZE 16
+#define RA_HEAD_DIM 128
+
+typedef enum {
+  RA_OK = 0,
+  RA_ERR_NULL = 1,        /* a required pointer is NULL */
+  RA_ERR_SHAPE = 2,       /* inconsistent sizes (negative, Hq % Hkv != 0, ...) */
+  RA_ERR_UNSUPPORTED = 3, /* valid but not built: page_size != 16, head_dim != 128,
+                             decode group size Hq / Hkv > 16 */
+  RA_ERR_WORKSPACE = 4,   /* workspace smaller than the *_workspace_size value */
+  RA_ERR_HIP = 5          /* a HIP launch failed (no device, bad stream, ...) */
+} ra_status;
+
+/* Caller-owned paged KV cache (device memory), see the layout above. */
+typedef struct {
+  void *k_pool;               /* bf16 [num_pages][num_kv_heads][page_size][head_dim] */
+  void *v_pool;               /* bf16 [num_pages][num_kv_heads][head_dim][page_size] */
+  const int32_t *block_table; /* int32 [B][bt_stride]; row b of the call's batch */
+  int32_t num_pages;
+  int32_t bt_stride;          /* entries per block-table row (>= 1) */
+  int32_t num_kv_heads;       /* Hkv */
+  int32_t page_size;          /* must be 16 */
+  int32_t head_dim;           /* must be 128 */
+} ra_paged_kv;
+
+/* ABI version of the loaded library (RA_ABI_VERSION). */
+int ra_abi_version(void);
+
+/* Static, human-readable name of a status code. */
+const char *ra_status_string(int status);
+
+/*
+ * Decode: one query token per trajectory against its cached keys
+ * (Sec. 3.3.2: each agent step is a completion over the full history).
+ * For row b and query head h with g = h / (Hq / Hkv):
+ *   out[b][h] = softmax_j(scale * <q[b][h], K_j>) · V_j over j in [0, kv_lens[b])
+ *   lse[b][h] = ln sum_j exp(scale * <q[b][h], K_j>)
+ * kv_lens counts the token being decoded (write it with kv_page_write first).
+ * Rows with kv_lens[b] <= 0 give out = 0 and lse = -inf.
+ *
+ *   q           bf16 [B][Hq][128]
+ *   kv          pools and block table ([B][bt_stride])
+ *   kv_lens     int32 [B]
+ *   max_kv_len  host: an upper bound of kv_lens (plans the split over pages);
+ *               must satisfy max_kv_len <= bt_stride * 16
+ *   out         fp32 [B][Hq][128]
+ *   lse         fp32 [B][Hq] or NULL
+ *   workspace   device scratch of at least
+ *               rollout_attn_decode_workspace_size(B, Hq, Hkv, max_kv_len) bytes
+ *               (split partial results; contents on entry are ignored)
+ * Errors: RA_ERR_NULL, RA_ERR_SHAPE (B < 0, Hq % Hkv, max_kv_len > bt_stride*16),
+ *         RA_ERR_UNSUPPORTED, RA_ERR_WORKSPACE, RA_ERR_HIP.
+ */
+size_t rollout_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
+                                          int32_t max_kv_len);
+int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_lens, int32_t B,
+                        int32_t Hq, int32_t max_kv_len, float scale, float *out, float *lse,
+                        void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Append: causal chunked prefill of newly appended observation tokens against
+ * each trajectory's cache (Sec. 3.3.3: earlier turns keep their tokens, new
+ * observations are tokenised and appended). Row b owns packed queries
+ * cu_q[b] .. cu_q[b+1]-1; its i-th query sits at absolute position
+ * ctx_lens[b] + i and attends keys 0 .. ctx_lens[b] + i (inclusive):
+ *   out[t][h] = softmax_j(scale * <q[t][h], K_j>) · V_j,  lse likewise.
+ * The chunk's own keys and values must already be in the pool at positions
+ * ctx_lens[b] .. ctx_lens[b] + T_b - 1 (kv_page_write with start_pos = ctx_lens
+ * on the same stream first).
+ *
+ *   q           bf16 [total_q][Hq][128]
+ *   cu_q        int32 [B+1], cu_q[0] = 0, cu_q[B] = total_q
+ *   ctx_lens    int32 [B]
+ *   max_q_len   host: an upper bound of T_b = cu_q[b+1] - cu_q[b]
+ *   max_kv_len  host: an upper bound of ctx_lens[b] + T_b; <= bt_stride * 16
+ *   out         fp32 [total_q][Hq][128]
+ *   lse         fp32 [total_q][Hq] or NULL
+ * Needs no workspace. Errors as for decode.
+ */
+int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_lens,
+                        const ra_paged_kv *kv, int32_t B, int32_t Hq, int32_t total_q,
+                        int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
+                        float *lse, hipStream_t stream);
+
+/*
+ * Page write: scatter new tokens' keys and values into their pages, a bit
+ * copy. Row b's new tokens are packed rows cu_new[b] .. cu_new[b+1]-1 of
+ * k_new / v_new; token t of the row goes to logical position start_pos[b] + t.
+ * No other pool byte changes. Rows of one call must not write the same slot.
+ *
+ *   k_new, v_new  bf16 [total_new][Hkv][128] (token-major)
+ *   cu_new        int32 [B+1]
+ *   start_pos     int32 [B]
+ *   max_new       host: an upper bound of cu_new[b+1] - cu_new[b]
+ *   max_pos       host: an upper bound of start_pos[b] + new tokens of row b;
+ *                 <= bt_stride * 16
+ */
+int kv_page_write(const void *k_new, const void *v_new, const int32_t *cu_new,
+                  const int32_t *start_pos, const ra_paged_kv *kv, int32_t B, int32_t total_new,
+                  int32_t max_new, int32_t max_pos, hipStream_t stream);
+
+/*
+ * Page gather (test and export helper): copy logical tokens 0 .. lens[b]-1 of
+ * every row out of the pages into packed token-major arrays; row b starts at
+ * packed row cu_out[b]. A bit copy.
+ *
+ *   lens     int32 [B]; max_len host upper bound of lens (<= bt_stride * 16)
+ *   cu_out   int32 [B+1]
+ *   k_out, v_out  bf16 [total][Hkv][128]
+ */
+int kv_page_gather(const ra_paged_kv *kv, const int32_t *lens, const int32_t *cu_out, int32_t B,
+                   int32_t total, int32_t max_len, void *k_out, void *v_out,
+                   hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROLLOUT_ATTN_H */

@@ -47,8 +47,15 @@ def _load():
     lib.oracle_page_gather.argtypes = [_u16p, _u16p, _i32p, c_i64, _i32p, _i32p, c_int, c_int,
                                        c_int, c_int, _u16p, _u16p]
     lib.oracle_page_gather.restype = c_int
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = c_int
     _lib = lib
     return lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().oracle_num_threads())
 
 
 def _u16(a):

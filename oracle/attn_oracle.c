@@ -41,6 +41,7 @@
  * Build: gcc -O2 -fopenmp -shared -fPIC (no -ffast-math), see oracle/build.py.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -243,3 +244,6 @@ int oracle_page_gather(const uint16_t *k_pool, const uint16_t *v_pool, const int
   }
   return 0;
 }
+
+/* Threads an OpenMP parallel region of the oracle uses (for reporting). */
+int oracle_num_threads(void) { return omp_get_max_threads(); }

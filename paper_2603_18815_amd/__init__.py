@@ -1,0 +1,223 @@
+"""MI355X rollout attention: paged-KV decode, observation append and page writes.
+
+Thin PyTorch-facing binding of the C ABI in include/rollout_attn.h. It only
+checks tensor dtypes/devices, allocates outputs with torch and passes raw
+device pointers plus torch's current HIP stream to the library; every step of
+the computation runs in the library's HIP kernels. If the library is not built
+the import of any function fails loudly: there is no fallback path.
+
+Layout (see the header): K pool bf16 [pages][Hkv][16][128] (token-major),
+V pool bf16 [pages][Hkv][128][16] (dim-major), block table int32 [B][stride].
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib
+from ._lib import RolloutAttnError  # noqa: F401  (re-export)
+
+PAGE_SIZE = 16
+HEAD_DIM = 128
+
+__all__ = ["PagedKV", "decode", "append", "kv_page_write", "kv_page_gather",
+           "decode_workspace_size", "abi_version", "RolloutAttnError"]
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, device: torch.device) -> None:
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _shape(t: torch.Tensor, shape, name: str) -> None:
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _rows(kv: "PagedKV", B: int) -> None:
+    if kv.block_table.shape[0] < B:
+        raise ValueError(f"block_table has {kv.block_table.shape[0]} rows, batch has {B}")
+
+
+def _stream(device: torch.device, stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+class PagedKV:
+    """A caller-owned paged KV cache: two pools and a block table, all on one GPU."""
+
+    def __init__(self, k_pool: torch.Tensor, v_pool: torch.Tensor, block_table: torch.Tensor):
+        dev = k_pool.device
+        _need(k_pool, "k_pool", torch.bfloat16, dev)
+        _need(v_pool, "v_pool", torch.bfloat16, dev)
+        _need(block_table, "block_table", torch.int32, dev)
+        if k_pool.dim() != 4 or k_pool.shape[2:] != (PAGE_SIZE, HEAD_DIM):
+            raise ValueError(f"k_pool must be [pages][Hkv][16][128], got {tuple(k_pool.shape)}")
+        n, hkv = k_pool.shape[:2]
+        if tuple(v_pool.shape) != (n, hkv, HEAD_DIM, PAGE_SIZE):
+            raise ValueError(f"v_pool must be [pages][Hkv][128][16], got {tuple(v_pool.shape)}")
+        if block_table.dim() != 2:
+            raise ValueError("block_table must be [B][stride]")
+        self.k_pool, self.v_pool, self.block_table = k_pool, v_pool, block_table
+        self.device = dev
+        self.num_pages, self.num_kv_heads = int(n), int(hkv)
+        self.bt_stride = int(block_table.shape[1])
+
+    def with_table(self, block_table: torch.Tensor) -> "PagedKV":
+        """Same pools, another block table (e.g. a sub-batch of rows)."""
+        return PagedKV(self.k_pool, self.v_pool, block_table)
+
+    def struct(self) -> _lib.RaPagedKV:
+        return _lib.RaPagedKV(self.k_pool.data_ptr(), self.v_pool.data_ptr(),
+                              self.block_table.data_ptr(), self.num_pages, self.bt_stride,
+                              self.num_kv_heads, PAGE_SIZE, HEAD_DIM)
+
+
+def abi_version() -> int:
+    return _lib.load().ra_abi_version()
+
+
+def decode_workspace_size(B: int, Hq: int, Hkv: int, max_kv_len: int) -> int:
+    return int(_lib.load().rollout_attn_decode_workspace_size(B, Hq, Hkv, max_kv_len))
+
+
+def decode(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor, max_kv_len: Optional[int] = None,
+           scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+           lse: Optional[torch.Tensor] = None, want_lse: bool = False,
+           workspace: Optional[torch.Tensor] = None, stream=None
+           ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Decode attention; q bf16 [B][Hq][128] -> out fp32 [B][Hq][128] (, lse fp32 [B][Hq])."""
+    lib = _lib.load()
+    dev = kv.device
+    _need(q, "q", torch.bfloat16, dev)
+    _need(kv_lens, "kv_lens", torch.int32, dev)
+    B, Hq, D = q.shape
+    _shape(q, (B, Hq, HEAD_DIM), "q")
+    _shape(kv_lens, (B,), "kv_lens")
+    _rows(kv, B)
+    if max_kv_len is None:
+        max_kv_len = int(kv_lens.max().item()) if B else 0
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, dev)
+    _shape(out, (B, Hq, HEAD_DIM), "out")
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+        _shape(lse, (B, Hq), "lse")
+    ws_bytes = lib.rollout_attn_decode_workspace_size(B, Hq, kv.num_kv_heads, max_kv_len)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    _need(workspace, "workspace", torch.uint8, dev)
+    s = kv.struct()
+    _lib.check("rollout_attn_decode", lib.rollout_attn_decode(
+        q.data_ptr(), ctypes.byref(s), kv_lens.data_ptr(), B, Hq, max_kv_len, float(scale),
+        out.data_ptr(), _ptr(lse), workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
+    return out, lse
+
+
+def append(q: torch.Tensor, cu_q: torch.Tensor, ctx_lens: torch.Tensor, kv: PagedKV,
+           max_q_len: Optional[int] = None, max_kv_len: Optional[int] = None,
+           scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+           lse: Optional[torch.Tensor] = None, want_lse: bool = False, stream=None
+           ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Append attention; q bf16 [total_q][Hq][128] -> out fp32 [total_q][Hq][128]."""
+    lib = _lib.load()
+    dev = kv.device
+    _need(q, "q", torch.bfloat16, dev)
+    _need(cu_q, "cu_q", torch.int32, dev)
+    _need(ctx_lens, "ctx_lens", torch.int32, dev)
+    total_q, Hq, D = q.shape
+    _shape(q, (total_q, Hq, HEAD_DIM), "q")
+    B = ctx_lens.shape[0]
+    _shape(cu_q, (B + 1,), "cu_q")
+    _rows(kv, B)
+    if max_q_len is None or max_kv_len is None:
+        t = (cu_q[1:] - cu_q[:-1]) if B else cu_q[:0]
+        if max_q_len is None:
+            max_q_len = int(t.max().item()) if B else 0
+        if max_kv_len is None:
+            max_kv_len = int((t + ctx_lens).max().item()) if B else 0
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty((total_q, Hq, D), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, dev)
+    _shape(out, (total_q, Hq, HEAD_DIM), "out")
+    if lse is None and want_lse:
+        lse = torch.empty((total_q, Hq), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+        _shape(lse, (total_q, Hq), "lse")
+    s = kv.struct()
+    _lib.check("rollout_attn_append", lib.rollout_attn_append(
+        q.data_ptr(), cu_q.data_ptr(), ctx_lens.data_ptr(), ctypes.byref(s), B, Hq, total_q,
+        max_q_len, max_kv_len, float(scale), out.data_ptr(), _ptr(lse), _stream(dev, stream)))
+    return out, lse
+
+
+def kv_page_write(k_new: torch.Tensor, v_new: torch.Tensor, cu_new: torch.Tensor,
+                  start_pos: torch.Tensor, kv: PagedKV, max_new: Optional[int] = None,
+                  max_pos: Optional[int] = None, stream=None) -> None:
+    """Scatter packed new tokens (bf16 [N][Hkv][128]) into the pages (bit copy)."""
+    lib = _lib.load()
+    dev = kv.device
+    _need(k_new, "k_new", torch.bfloat16, dev)
+    _need(v_new, "v_new", torch.bfloat16, dev)
+    _need(cu_new, "cu_new", torch.int32, dev)
+    _need(start_pos, "start_pos", torch.int32, dev)
+    B = start_pos.shape[0]
+    _shape(cu_new, (B + 1,), "cu_new")
+    _shape(k_new, (k_new.shape[0], kv.num_kv_heads, HEAD_DIM), "k_new")
+    _shape(v_new, tuple(k_new.shape), "v_new")
+    _rows(kv, B)
+    if max_new is None or max_pos is None:
+        n = (cu_new[1:] - cu_new[:-1]) if B else cu_new[:0]
+        if max_new is None:
+            max_new = int(n.max().item()) if B else 0
+        if max_pos is None:
+            max_pos = int((n + start_pos).max().item()) if B else 0
+    s = kv.struct()
+    _lib.check("kv_page_write", lib.kv_page_write(
+        k_new.data_ptr(), v_new.data_ptr(), cu_new.data_ptr(), start_pos.data_ptr(),
+        ctypes.byref(s), B, k_new.shape[0], max_new, max_pos, _stream(dev, stream)))
+
+
+def kv_page_gather(kv: PagedKV, lens: torch.Tensor, cu_out: torch.Tensor,
+                   total: Optional[int] = None, max_len: Optional[int] = None, stream=None
+                   ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Copy logical tokens [0, lens[b]) of every row out to packed bf16 [total][Hkv][128]."""
+    lib = _lib.load()
+    dev = kv.device
+    _need(lens, "lens", torch.int32, dev)
+    _need(cu_out, "cu_out", torch.int32, dev)
+    B = lens.shape[0]
+    _shape(cu_out, (B + 1,), "cu_out")
+    _rows(kv, B)
+    if total is None:
+        total = int(cu_out[-1].item()) if B else 0
+    if max_len is None:
+        max_len = int(lens.max().item()) if B else 0
+    k_out = torch.empty((total, kv.num_kv_heads, HEAD_DIM), dtype=torch.bfloat16, device=dev)
+    v_out = torch.empty_like(k_out)
+    s = kv.struct()
+    _lib.check("kv_page_gather", lib.kv_page_gather(
+        ctypes.byref(s), lens.data_ptr(), cu_out.data_ptr(), B, total, max_len,
+        k_out.data_ptr(), v_out.data_ptr(), _stream(dev, stream)))
+    return k_out, v_out

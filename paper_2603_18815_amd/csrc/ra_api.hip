@@ -1,0 +1,125 @@
+// C ABI of the rollout-attention library: argument validation (before any HIP
+// call), launch planning and status codes. See include/rollout_attn.h.
+#include "rollout_attn.h"
+
+#include "ra_internal.h"
+
+namespace {
+
+constexpr int32_t kMaxGridYZ = 65535;
+
+bool valid_status(int s) { return s >= RA_OK && s <= RA_ERR_HIP; }
+
+// Common checks on the paged cache descriptor.
+int check_kv(const ra_paged_kv *kv) {
+  if (!kv) return RA_ERR_NULL;
+  if (kv->page_size != RA_PAGE_SIZE || kv->head_dim != RA_HEAD_DIM) return RA_ERR_UNSUPPORTED;
+  if (kv->num_kv_heads <= 0 || kv->num_pages <= 0 || kv->bt_stride <= 0) return RA_ERR_SHAPE;
+  if (kv->num_kv_heads > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!kv->k_pool || !kv->v_pool || !kv->block_table) return RA_ERR_NULL;
+  return RA_OK;
+}
+
+bool positions_fit(const ra_paged_kv *kv, int32_t max_pos) {
+  return max_pos >= 0 && (int64_t)max_pos <= (int64_t)kv->bt_stride * RA_PAGE_SIZE;
+}
+
+ra::PagedKV to_internal(const ra_paged_kv *kv) {
+  ra::PagedKV p;
+  p.k_pool = static_cast<uint16_t *>(kv->k_pool);
+  p.v_pool = static_cast<uint16_t *>(kv->v_pool);
+  p.block_table = kv->block_table;
+  p.num_pages = kv->num_pages;
+  p.bt_stride = kv->bt_stride;
+  p.hkv = kv->num_kv_heads;
+  return p;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? RA_OK : RA_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int ra_abi_version(void) { return RA_ABI_VERSION; }
+
+const char *ra_status_string(int status) {
+  static const char *names[] = {"RA_OK", "RA_ERR_NULL", "RA_ERR_SHAPE", "RA_ERR_UNSUPPORTED",
+                                "RA_ERR_WORKSPACE", "RA_ERR_HIP"};
+  return valid_status(status) ? names[status] : "RA_UNKNOWN_STATUS";
+}
+
+size_t rollout_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
+                                          int32_t max_kv_len) {
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || max_kv_len < 0) return 0;
+  return ra::decode_workspace_bytes(B, Hq, ra::decode_plan(B, Hkv, max_kv_len));
+}
+
+int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_lens, int32_t B,
+                        int32_t Hq, int32_t max_kv_len, float scale, float *out, float *lse,
+                        void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (B < 0 || Hq <= 0 || max_kv_len < 0) return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!q || !kv_lens || !out) return RA_ERR_NULL;
+  if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
+  if (Hq / kv->num_kv_heads > 16 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_kv_len)) return RA_ERR_SHAPE;
+  if (B == 0) return RA_OK;
+  const ra::DecodePlan plan = ra::decode_plan(B, kv->num_kv_heads, max_kv_len);
+  if (!workspace || workspace_bytes < ra::decode_workspace_bytes(B, Hq, plan))
+    return RA_ERR_WORKSPACE;
+  return hip_status(ra::launch_decode(static_cast<const uint16_t *>(q), to_internal(kv), kv_lens,
+                                      B, Hq, max_kv_len, scale, out, lse, workspace, plan,
+                                      stream));
+}
+
+int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_lens,
+                        const ra_paged_kv *kv, int32_t B, int32_t Hq, int32_t total_q,
+                        int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
+                        float *lse, hipStream_t stream) {
+  if (B < 0 || Hq <= 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0) return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!q || !cu_q || !ctx_lens || !out) return RA_ERR_NULL;
+  if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
+  if (Hq / kv->num_kv_heads > 256 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_kv_len) || max_q_len > max_kv_len) return RA_ERR_SHAPE;
+  if (B == 0 || total_q == 0 || max_q_len == 0) return RA_OK;
+  return hip_status(ra::launch_append(static_cast<const uint16_t *>(q), cu_q, ctx_lens,
+                                      to_internal(kv), B, Hq, total_q, max_q_len, max_kv_len,
+                                      scale, out, lse, stream));
+}
+
+int kv_page_write(const void *k_new, const void *v_new, const int32_t *cu_new,
+                  const int32_t *start_pos, const ra_paged_kv *kv, int32_t B, int32_t total_new,
+                  int32_t max_new, int32_t max_pos, hipStream_t stream) {
+  if (B < 0 || total_new < 0 || max_new < 0 || max_pos < 0) return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!k_new || !v_new || !cu_new || !start_pos) return RA_ERR_NULL;
+  if (B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_pos) || max_new > max_pos) return RA_ERR_SHAPE;
+  if (B == 0 || total_new == 0 || max_new == 0) return RA_OK;
+  return hip_status(ra::launch_page_write(static_cast<const uint16_t *>(k_new),
+                                          static_cast<const uint16_t *>(v_new), cu_new, start_pos,
+                                          to_internal(kv), B, total_new, max_new, max_pos,
+                                          stream));
+}
+
+int kv_page_gather(const ra_paged_kv *kv, const int32_t *lens, const int32_t *cu_out, int32_t B,
+                   int32_t total, int32_t max_len, void *k_out, void *v_out,
+                   hipStream_t stream) {
+  if (B < 0 || total < 0 || max_len < 0) return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!lens || !cu_out || !k_out || !v_out) return RA_ERR_NULL;
+  if (B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_len)) return RA_ERR_SHAPE;
+  if (B == 0 || total == 0 || max_len == 0) return RA_OK;
+  return hip_status(ra::launch_page_gather(to_internal(kv), lens, cu_out, B, total, max_len,
+                                           static_cast<uint16_t *>(k_out),
+                                           static_cast<uint16_t *>(v_out), stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,71 @@
+// Device-side helpers shared by the rollout-attention kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ra {
+
+constexpr int kPage = 16;        // tokens per page
+constexpr int kHeadDim = 128;    // head dimension
+constexpr int kWave = 64;        // CDNA wavefront width
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte global load of 8 bf16 (one dwordx4 per lane).
+__device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t *p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+}
+
+__device__ __forceinline__ u32x4 load_u32x4(const uint16_t *p) {
+  return *reinterpret_cast<const u32x4 *>(p);
+}
+
+__device__ __forceinline__ void store_u32x4(uint16_t *p, u32x4 v) {
+  *reinterpret_cast<u32x4 *>(p) = v;
+}
+
+// D(16x16, fp32) += A(16x32, bf16) * B(32x16, bf16) on the matrix cores.
+// Lane l supplies A row (l % 16) and B column (l % 16), eight consecutive
+// contraction slots each (slot group l / 16); it receives D rows
+// 4 * (l / 16) + 0..3 of column l % 16.
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Round 8 fp32 values to bf16 (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ bf16x8 to_bf16x8(f32x8 v) {
+  return __builtin_convertvector(v, bf16x8);
+}
+
+__device__ __forceinline__ f32x8 to_f32x8(bf16x8 v) {
+  return __builtin_convertvector(v, f32x8);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Max / sum over the four lanes that share a matrix column (lanes l, l^16,
+// l^32, l^48).
+__device__ __forceinline__ float col_max4(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+
+__device__ __forceinline__ float col_sum4(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+__device__ __forceinline__ int clamp_page(int id, int num_pages) {
+  return min(max(id, 0), num_pages - 1);
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+}  // namespace ra

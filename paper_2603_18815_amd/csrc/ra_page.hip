@@ -1,0 +1,120 @@
+// Page write and page gather: bit copies between packed token-major K/V rows
+// and the paged pools (K pages token-major [16][128], V pages dim-major
+// [128][16]). One workgroup moves one (row, page, KV head) block of 4 KiB per
+// pool; V goes through LDS so that both sides are accessed 16 bytes per lane.
+#include "ra_device.h"
+#include "ra_internal.h"
+
+namespace ra {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kVPitch = kHeadDim + 8;  // LDS row pitch (elements) of the staged V slots
+
+__global__ __launch_bounds__(kThreads) void page_write_kernel(
+    const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
+    const int32_t *__restrict__ cu_new, const int32_t *__restrict__ start_pos,
+    uint16_t *__restrict__ k_pool, uint16_t *__restrict__ v_pool,
+    const int32_t *__restrict__ block_table, int bt_stride, int num_pages, int hkv,
+    int total_new, int max_new, int max_pos) {
+  const int chunk = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  // Row extent, clamped so that no access leaves the caller's arrays.
+  const int cu0 = min(max(cu_new[b], 0), total_new);
+  const int n = min(min(max(cu_new[b + 1] - cu0, 0), max_new), total_new - cu0);
+  if (n <= 0) return;
+  const int s = min(max(start_pos[b], 0), max_pos - n);
+  if (s < 0) return;
+  const int pg = s / kPage + chunk;                   // row-relative page
+  if (pg > (s + n - 1) / kPage) return;
+  const int lo = max(s, pg * kPage), hi = min(s + n, pg * kPage + kPage);
+  const int id = clamp_page(block_table[(size_t)b * bt_stride + pg], num_pages);
+
+  __shared__ uint16_t sv[kPage][kVPitch];
+  const int slot = tid >> 4, ch = tid & 15;            // token slot, 16-byte chunk
+  const int pos = pg * kPage + slot;
+  const bool live = pos >= lo && pos < hi;
+  if (live) {
+    const size_t src = ((size_t)(cu0 + pos - s) * hkv + g) * kHeadDim + ch * 8;
+    const size_t dst = (((size_t)id * hkv + g) * kPage + slot) * kHeadDim + ch * 8;
+    store_u32x4(k_pool + dst, load_u32x4(k_new + src));
+    *reinterpret_cast<u32x4 *>(&sv[slot][ch * 8]) = load_u32x4(v_new + src);
+  }
+  __syncthreads();
+  // V page is [d][slot]: thread -> one d row, eight slots.
+  const int d = tid >> 1, s0 = (tid & 1) * 8;
+  uint16_t *dst = v_pool + (((size_t)id * hkv + g) * kHeadDim + d) * kPage + s0;
+  const int p0 = pg * kPage + s0;
+  if (p0 >= lo && p0 + 8 <= hi) {
+    uint16_t t[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[e] = sv[s0 + e][d];
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)t[2 * e] | ((uint32_t)t[2 * e + 1] << 16);
+    store_u32x4(dst, w);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (p0 + e >= lo && p0 + e < hi) dst[e] = sv[s0 + e][d];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void page_gather_kernel(
+    const uint16_t *__restrict__ k_pool, const uint16_t *__restrict__ v_pool,
+    const int32_t *__restrict__ block_table, int bt_stride, int num_pages, int hkv,
+    const int32_t *__restrict__ lens, const int32_t *__restrict__ cu_out, int total, int max_len,
+    uint16_t *__restrict__ k_out, uint16_t *__restrict__ v_out) {
+  const int pg = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int cu0 = min(max(cu_out[b], 0), total);
+  const int L = min(min(max(lens[b], 0), max_len), total - cu0);
+  if (pg * kPage >= L) return;
+  const int id = clamp_page(block_table[(size_t)b * bt_stride + pg], num_pages);
+
+  __shared__ uint16_t sv[kPage][kVPitch];
+  {
+    const int d = tid >> 1, s0 = (tid & 1) * 8;
+    const u32x4 w = load_u32x4(v_pool + (((size_t)id * hkv + g) * kHeadDim + d) * kPage + s0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      sv[s0 + 2 * e][d] = (uint16_t)(w[e] & 0xffffu);
+      sv[s0 + 2 * e + 1][d] = (uint16_t)(w[e] >> 16);
+    }
+  }
+  __syncthreads();
+  const int slot = tid >> 4, ch = tid & 15;
+  const int pos = pg * kPage + slot;
+  if (pos < L) {
+    const size_t dst = ((size_t)(cu0 + pos) * hkv + g) * kHeadDim + ch * 8;
+    const size_t src = (((size_t)id * hkv + g) * kPage + slot) * kHeadDim + ch * 8;
+    store_u32x4(k_out + dst, load_u32x4(k_pool + src));
+    store_u32x4(v_out + dst, *reinterpret_cast<const u32x4 *>(&sv[slot][ch * 8]));
+  }
+}
+
+}  // namespace
+
+hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
+                             const int32_t *start_pos, const PagedKV &kv, int32_t B,
+                             int32_t total_new, int32_t max_new, int32_t max_pos,
+                             hipStream_t stream) {
+  // A run of n tokens touches at most (n - 1) / 16 + 2 pages.
+  const dim3 grid((max_new + kPage - 1) / kPage + 1, kv.hkv, B);
+  hipLaunchKernelGGL(page_write_kernel, grid, dim3(kThreads), 0, stream, k_new, v_new, cu_new,
+                     start_pos, kv.k_pool, kv.v_pool, kv.block_table, kv.bt_stride, kv.num_pages,
+                     kv.hkv, total_new, max_new, max_pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_page_gather(const PagedKV &kv, const int32_t *lens, const int32_t *cu_out,
+                              int32_t B, int32_t total, int32_t max_len, uint16_t *k_out,
+                              uint16_t *v_out, hipStream_t stream) {
+  const dim3 grid((max_len + kPage - 1) / kPage, kv.hkv, B);
+  hipLaunchKernelGGL(page_gather_kernel, grid, dim3(kThreads), 0, stream, kv.k_pool, kv.v_pool,
+                     kv.block_table, kv.bt_stride, kv.num_pages, kv.hkv, lens, cu_out, total,
+                     max_len, k_out, v_out);
+  return hipGetLastError();
+}
+
+}  // namespace ra

@@ -256,3 +256,32 @@ def poison_unowned(k_pool: torch.Tensor, v_pool: torch.Tensor, layout: PagedLayo
             page = int(layout.block_table[r, L // P])
             k_pool[page, :, L % P:, :] = nan
             v_pool[page, :, :, L % P:] = nan
+
+
+# ---------------------------------------------------------------------------
+# Host copies (for the CPU oracle): bit patterns and the pages of a few rows
+# ---------------------------------------------------------------------------
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    """bf16 tensor (any device) -> host uint16 bit patterns."""
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def compact_rows(k_pool: torch.Tensor, v_pool: torch.Tensor, table: np.ndarray, lens):
+    """Host copy of only the pages the given rows use, with a remapped block table.
+
+    table: [R][stride] block-table rows; lens: tokens used per row. The copy is
+    made with torch indexing.
+    """
+    P = k_pool.shape[2]
+    pages = [table[r, :(int(L) + P - 1) // P] for r, L in enumerate(lens)]
+    ids = np.unique(np.concatenate(pages)) if pages else np.zeros(0, np.int64)
+    idx = torch.as_tensor(ids.astype(np.int64), device=k_pool.device)
+    k = bits(k_pool.index_select(0, idx))
+    v = bits(v_pool.index_select(0, idx))
+    remap = {int(p): i for i, p in enumerate(ids)}
+    stride = max(1, max(len(p) for p in pages)) if pages else 1
+    bt = np.zeros((len(pages), stride), np.int32)
+    for r, p in enumerate(pages):
+        bt[r, :len(p)] = [remap[int(x)] for x in p]
+    return k, v, bt

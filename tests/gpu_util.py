@@ -1,0 +1,42 @@
+"""Helpers for the GPU parity tests: host copies for the oracle and the tolerance check.
+
+Tolerance (bf16 inputs, fp32 accumulation): over each compared output tensor,
+max |gpu - oracle| <= 1e-2 and ||gpu - oracle||_2 / ||oracle||_2 <= 5e-3.
+"""
+import numpy as np
+
+from synth import bits, compact_rows  # noqa: F401  (re-export)
+
+MAX_ABS = 1e-2
+REL_L2 = 5e-3
+
+
+def attn_stats(gpu, ref):
+    g = np.asarray(gpu, np.float64)
+    r = np.asarray(ref, np.float64)
+    diff = g - r
+    max_abs = float(np.abs(diff).max()) if diff.size else 0.0
+    rel = float(np.linalg.norm(diff) / max(np.linalg.norm(r), 1e-300)) if diff.size else 0.0
+    return max_abs, rel
+
+
+def assert_attn_close(gpu, ref, what: str = ""):
+    g = np.asarray(gpu, np.float64)
+    assert np.all(np.isfinite(g)), f"{what}: non-finite output"
+    max_abs, rel = attn_stats(g, ref)
+    print(f"[parity] {what}: max_abs={max_abs:.3e} rel_l2={rel:.3e}", flush=True)
+    assert max_abs <= MAX_ABS and rel <= REL_L2, (what, max_abs, rel)
+    return max_abs, rel
+
+
+def sample_rows(lens, k: int, seed: int):
+    """The longest row, the shortest row and k - 2 seeded random others."""
+    lens = np.asarray(lens)
+    n = lens.shape[0]
+    rng = np.random.default_rng(seed)
+    pick = {int(np.argmax(lens)), int(np.argmin(lens))}
+    for r in rng.permutation(n):
+        if len(pick) >= min(k, n):
+            break
+        pick.add(int(r))
+    return np.array(sorted(pick), np.int64)

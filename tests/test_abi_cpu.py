@@ -1,0 +1,116 @@
+"""C ABI checks that need no GPU: the library loads, exports every declared
+symbol, and rejects bad arguments before touching HIP (CPU only)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2603_18815_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rollout_attn.h")
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def _kv(**kw):
+    d = dict(k_pool=FAKE, v_pool=FAKE, block_table=FAKE, num_pages=10, bt_stride=4,
+             num_kv_heads=2, page_size=16, head_dim=128)
+    d.update(kw)
+    return _lib.RaPagedKV(**d)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert set(names) == set(_lib.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_abi_version_and_status_strings(lib):
+    assert lib.ra_abi_version() == 1
+    assert lib.ra_status_string(0) == b"RA_OK"
+    assert lib.ra_status_string(4) == b"RA_ERR_WORKSPACE"
+    assert lib.ra_status_string(99) == b"RA_UNKNOWN_STATUS"
+
+
+def test_workspace_size(lib):
+    f = lib.rollout_attn_decode_workspace_size
+    assert f(0, 32, 8, 1000) == 0
+    a = f(64, 32, 8, 32768)
+    assert a > 0 and a % 4 == 0
+    assert f(64, 32, 8, 65536) >= a          # longer rows need at least as many splits
+    assert f(128, 32, 8, 32768) >= a
+
+
+def _decode(lib, kv, **kw):
+    d = dict(q=FAKE, kv_lens=FAKE, B=2, Hq=4, max_kv_len=64, scale=0.1, out=FAKE, lse=None,
+             ws=FAKE, ws_bytes=1 << 30, stream=None)
+    d.update(kw)
+    return lib.rollout_attn_decode(d["q"], ctypes.byref(kv), d["kv_lens"], d["B"], d["Hq"],
+                                   d["max_kv_len"], d["scale"], d["out"], d["lse"], d["ws"],
+                                   d["ws_bytes"], d["stream"])
+
+
+def test_decode_validation(lib):
+    assert _decode(lib, _kv(), q=None) == _lib.RA_ERR_NULL
+    assert _decode(lib, _kv(), out=None) == _lib.RA_ERR_NULL
+    assert _decode(lib, _kv(k_pool=None)) == _lib.RA_ERR_NULL
+    assert _decode(lib, _kv(), B=-1) == _lib.RA_ERR_SHAPE
+    assert _decode(lib, _kv(), Hq=3) == _lib.RA_ERR_SHAPE                 # Hq % Hkv
+    assert _decode(lib, _kv(), max_kv_len=65) == _lib.RA_ERR_SHAPE        # > bt_stride * 16
+    assert _decode(lib, _kv(page_size=32)) == _lib.RA_ERR_UNSUPPORTED
+    assert _decode(lib, _kv(head_dim=64)) == _lib.RA_ERR_UNSUPPORTED
+    assert _decode(lib, _kv(), Hq=34) == _lib.RA_ERR_UNSUPPORTED          # group of 17
+    assert _decode(lib, _kv(), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
+    assert _decode(lib, _kv(), ws=None) == _lib.RA_ERR_WORKSPACE
+    assert _decode(lib, _kv(), B=0) == _lib.RA_OK                         # no work, no launch
+
+
+def test_append_validation(lib):
+    def call(kv, **kw):
+        d = dict(q=FAKE, cu=FAKE, ctx=FAKE, B=2, Hq=4, total_q=10, max_q=5, max_kv=64,
+                 out=FAKE)
+        d.update(kw)
+        return lib.rollout_attn_append(d["q"], d["cu"], d["ctx"], ctypes.byref(kv), d["B"],
+                                       d["Hq"], d["total_q"], d["max_q"], d["max_kv"], 0.1,
+                                       d["out"], None, None)
+    assert call(_kv(), cu=None) == _lib.RA_ERR_NULL
+    assert call(_kv(), total_q=-1) == _lib.RA_ERR_SHAPE
+    assert call(_kv(), max_kv=100) == _lib.RA_ERR_SHAPE
+    assert call(_kv(), max_q=70, max_kv=64) == _lib.RA_ERR_SHAPE
+    assert call(_kv(), Hq=5) == _lib.RA_ERR_SHAPE
+    assert call(_kv(head_dim=256)) == _lib.RA_ERR_UNSUPPORTED
+    assert call(_kv(), total_q=0) == _lib.RA_OK
+    assert call(_kv(), B=0) == _lib.RA_OK
+
+
+def test_page_write_and_gather_validation(lib):
+    kv = _kv()
+    w = lambda **kw: lib.kv_page_write(kw.get("k", FAKE), FAKE, FAKE, FAKE, ctypes.byref(
+        kw.get("kv", kv)), kw.get("B", 2), kw.get("total", 8), kw.get("max_new", 4),
+        kw.get("max_pos", 64), None)
+    assert w(k=None) == _lib.RA_ERR_NULL
+    assert w(max_pos=65) == _lib.RA_ERR_SHAPE
+    assert w(max_new=70) == _lib.RA_ERR_SHAPE
+    assert w(kv=_kv(num_kv_heads=0)) == _lib.RA_ERR_SHAPE
+    assert w(total=0) == _lib.RA_OK
+    g = lambda **kw: lib.kv_page_gather(ctypes.byref(kw.get("kv", kv)), FAKE, FAKE,
+                                        kw.get("B", 2), 8, kw.get("max_len", 64),
+                                        kw.get("k", FAKE), FAKE, None)
+    assert g(k=None) == _lib.RA_ERR_NULL
+    assert g(max_len=100) == _lib.RA_ERR_SHAPE
+    assert g(kv=_kv(page_size=8)) == _lib.RA_ERR_UNSUPPORTED
+    assert g(B=0) == _lib.RA_OK
