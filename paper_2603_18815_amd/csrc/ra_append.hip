@@ -1,34 +1,41 @@
 // Append attention: causal chunked prefill of new observation tokens against
 // each trajectory's paged cache.
 //
-// One workgroup (4 waves) owns a block of QB = 256 / G consecutive queries of
-// one row and all G query heads of one KV head: 256 "query rows" (query,
-// head), 64 per wave, as four 16-wide matrix columns per wave. The key loop
-// walks the row's pages 64 keys (4 pages) at a time; each block of K and V is
-// staged once in LDS (double buffered, one barrier per block) and consumed by
-// all four waves from there:
-//   S^T[key][qrow] = K[key][:] · Q^T[:][qrow]        (bf16 mfma 16x16x32, fp32)
+// One workgroup (8 waves, two per SIMD) owns a block of QB = 256 / G
+// consecutive queries of one row and all G query heads of one KV head: 256
+// "query rows" (query, head), 32 per wave, each wave's rows forming the 32
+// columns of its 32x32 matrix tiles with their Q^T operands in registers.
+// The key loop walks the row's pages 64 keys (4 pages) at a time. Each block
+// of K and V is loaded once per workgroup into registers, stored to one of
+// two LDS buffers (the load of the next block is in flight while the current
+// one is used), one barrier per block, and all eight waves consume it:
+//   S^T[key][qrow] = K[key][:] · Q^T[:][qrow]        (bf16 mfma 32x32x16, fp32)
 //   O^T[d][qrow]  += V^T[d][key] · P^T[key][qrow]    (P rounded to bf16)
-// Every K or V operand read from LDS feeds four matrix products (the wave's
-// four columns). Keys are ordered inside each pair of pages so that a lane's
-// S values are exactly the P^T operand it supplies next (no shuffles), and
-// O^T keeps each query row in one lane column so that the online-softmax
-// rescale is lane-local. The causal mask (key position > ctx + i) is applied
-// only on blocks that reach past the wave's first query position.
+// Keys are ordered inside each pair of pages so that the 16 S values a lane
+// receives are, in order, 8 consecutive slots of the first page and the same
+// 8 slots of the second: exactly the P^T operands of the two P·V products it
+// takes part in (no shuffles). Each query row stays in one lane column (two
+// lanes), so the online-softmax state is lane-local and the column max needs
+// a single cross-lane exchange. The causal mask (key position > ctx + i) is
+// applied only on blocks that reach past the wave's first query position.
 #include "ra_device.h"
 #include "ra_internal.h"
 
 namespace ra {
 namespace {
 
-constexpr int kWaves = 4;
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * kWave;
-constexpr int kCols = 4;                  // 16-wide matrix columns per wave
-constexpr int kRowsPerWave = 16 * kCols;  // query rows per wave
-constexpr int kRowsPerGroup = kWaves * kRowsPerWave;
-constexpr int kBlock = 64;                // keys per staged block
-constexpr int kBlockPages = kBlock / kPage;   // = kWaves: wave w stages page w
-constexpr float kSlack = 8.f;             // lazy-rescale threshold (base-2 units)
+constexpr int kRowsPerWave = 32;
+constexpr int kRowsPerGroup = kWaves * kRowsPerWave;   // 256
+constexpr int kBlock = 64;                             // keys per staged block
+constexpr int kBlockPages = kBlock / kPage;            // 4
+constexpr int kPagesPerPass = kThreads / 256;          // pages one staging pass covers
+constexpr int kPasses = kBlockPages / kPagesPerPass;   // 2
+constexpr int kBlockElems = kBlock * kHeadDim;         // per pool, per buffer
+constexpr float kSlack = 8.f;                          // lazy-rescale threshold (base 2)
 
 struct AppendArgs {
   const uint16_t *q;
@@ -43,20 +50,35 @@ struct AppendArgs {
   float scale_log2;
 };
 
-// K block in LDS: 64 key rows of 128 dims (256 B, no padding). The 16-byte
-// chunk c of row R is stored at chunk c ^ swz(R): the 16 rows read together
-// by one matrix operand load then fall on 16 distinct bank groups.
-__device__ __forceinline__ int k_swz(int row) { return (row & 3) | (((row >> 3) & 3) << 2); }
+// D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16). Lane l supplies A row
+// (l % 32) and B column (l % 32), contraction slots 8 (l / 32) + 0..7; it
+// receives D rows 8 (r / 4) + 4 (l / 32) + r % 4 of column l % 32, r = 0..15.
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
 
-// V block in LDS: [page][d][16 slots]; the two 8-slot halves of row d are
-// swapped when bit 3 of d is set, for the same reason.
-__device__ __forceinline__ int v_half(int d, int half) { return half ^ ((d >> 3) & 1); }
+__device__ __forceinline__ bf16x8 lds_bf16x8(const uint16_t *p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+}
 
+// LDS layouts (per buffer). K: 64 key rows x 128 dims (256 B rows); the
+// 16-byte chunk c of row R sits at chunk c ^ (R & 15), so the 16 rows that
+// one quarter-wave reads fall on distinct banks. V: [page][d][16 slots]
+// (32 B rows); the two 8-slot halves of row d are swapped when bit 3 of d is
+// set, for the same reason.
+__device__ __forceinline__ int k_lds(int row, int chunk) {
+  return row * kHeadDim + ((chunk ^ (row & 15)) * 8);
+}
+__device__ __forceinline__ int v_lds(int page, int d, int half) {
+  return (page * kHeadDim + d) * kPage + ((half ^ ((d >> 3) & 1)) * 8);
+}
+
+template <bool kPosScale>
 __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
   const int qblk = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1), wave = tid / kWave;
-  const int col = lane & 15, kgrp = lane >> 4;
+  const int col = lane & 31, grp = lane >> 5;
   const int G = a.group, QB = a.q_per_block;
 
   // Row extent, clamped so that no access leaves the caller's arrays.
@@ -74,193 +96,182 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
   const int32_t *bt = a.block_table + (size_t)b * a.bt_stride;
   const size_t head_stride = (size_t)kPage * kHeadDim;
 
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBlock * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBlockPages * kHeadDim * kPage];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2 * kBlockElems];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2 * kBlockElems];
 
-  // ---- this lane's query rows and Q^T operands ----
-  int qpos[kCols];
-  bf16x8 qop[kCols][4];
+  // ---- this lane's query row and Q^T operands (dims 16 kk + 8 grp + 0..7) ----
+  const int r_wg = wave * kRowsPerWave + col;
+  const int qi = r_wg / G, hh = r_wg - qi * G;
+  const bool q_valid = r_wg < QB * G && i0 + qi < i_end;
+  const int qpos = q_valid ? ctx + i0 + qi : -1;
+  bf16x8 qop[8];
+  if (q_valid) {
+    const uint16_t *qp =
+        a.q + ((size_t)(cu0 + i0 + qi) * a.hq + (size_t)g * G + hh) * kHeadDim + 8 * grp;
 #pragma unroll
-  for (int nt = 0; nt < kCols; ++nt) {
-    const int r = wave * kRowsPerWave + nt * 16 + col;
-    const int qi = r / G, hh = r - qi * G;
-    const bool valid = r < QB * G && i0 + qi < i_end;
-    qpos[nt] = valid ? ctx + i0 + qi : -1;
-    if (valid) {
-      const uint16_t *qp =
-          a.q + ((size_t)(cu0 + i0 + qi) * a.hq + (size_t)g * G + hh) * kHeadDim + 8 * kgrp;
+    for (int kk = 0; kk < 8; ++kk) qop[kk] = load_bf16x8(qp + 16 * kk);
+  } else {
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = load_bf16x8(qp + 32 * kk);
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = bf16x8{};
-    }
+    for (int kk = 0; kk < 8; ++kk) qop[kk] = bf16x8{};
   }
   // First query position of this wave (its rows are query-major).
   const int wave_q0 = ctx + i0 + (wave * kRowsPerWave) / G;
 
-  // ---- staging: wave w copies page w of each block, K and V, straight
-  // from HBM into LDS (global_load_lds, 16 bytes per lane, no registers).
-  // The LDS destination of a lane is fixed (base + 16 * lane), so the swizzled
-  // layout is produced by choosing which global chunk each lane fetches.
-  // Slots past the row's end are not cleared here; their scores are always
-  // masked (they lie beyond every query of the row) and their V entries are
-  // replaced by zero when read (last block only).
-  const int kr = lane >> 4, kpc = lane & 15;          // K: row in a 4-row chunk, phys. chunk
-  const int vd = lane >> 1, vph = lane & 1;           // V: row in a 32-row chunk, phys. half
-  auto stage = [&](int blk, int buf) {
-    const int pgi = blk * kBlockPages + wave;
-    const int id = clamp_page(pgi < row_pages ? bt[pgi] : bt[0], a.num_pages);
-    const size_t base = ((size_t)id * a.hkv + g) * head_stride;
+  // ---- staging: pass p moves pages 2p, 2p + 1 of the block; each thread one
+  // 16-byte chunk of K and one of V.
+  const int st_page = tid >> 8, st_chunk = tid & 255;
+  const int st_slot = st_chunk >> 4, st_kch = st_chunk & 15;   // K: slot, 16-B chunk
+  const int st_d = st_chunk >> 1, st_half = st_chunk & 1;      // V: dim row, 8-slot half
+  u32x4 kreg[kPasses], vreg[kPasses];
+  auto stage_load = [&](int blk) __attribute__((always_inline)) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int row = wave * kPage + 4 * c + kr;      // row in the block
-      const uint16_t *src = a.k_pool + base + (4 * c + kr) * kHeadDim + ((kpc ^ k_swz(row)) * 8);
-      __builtin_amdgcn_global_load_lds(src, &sK[buf][(wave * kPage + 4 * c) * kHeadDim], 16, 0,
-                                       0);
+    for (int p = 0; p < kPasses; ++p) {
+      const int pgi = blk * kBlockPages + p * kPagesPerPass + st_page;
+      const int id = clamp_page(pgi < row_pages ? bt[pgi] : bt[0], a.num_pages);
+      const size_t base = ((size_t)id * a.hkv + g) * head_stride;
+      kreg[p] = load_u32x4(a.k_pool + base + st_slot * kHeadDim + st_kch * 8);
+      vreg[p] = load_u32x4(a.v_pool + base + st_d * kPage + st_half * 8);
     }
+  };
+  auto stage_store = [&](int blk, int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int d = 32 * c + vd;
-      const uint16_t *src = a.v_pool + base + d * kPage + v_half(d, vph) * 8;
-      __builtin_amdgcn_global_load_lds(src, &sV[buf][(wave * kHeadDim + 32 * c) * kPage], 16, 0,
-                                       0);
+    for (int p = 0; p < kPasses; ++p) {
+      const int j = p * kPagesPerPass + st_page;        // page in the block
+      const int pos0 = (blk * kBlockPages + j) * kPage;
+      // Slots at or past the row's end may hold anything: store zeros instead.
+      u32x4 kw = kreg[p], vw = vreg[p];
+      if (pos0 + st_slot >= row_end) kw = u32x4{0u, 0u, 0u, 0u};
+      const int vpos = pos0 + st_half * 8;
+      if (vpos + 8 > row_end) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = vpos + 2 * e < row_end ? 0xffffu : 0u;
+          const uint32_t hi = vpos + 2 * e + 1 < row_end ? 0xffff0000u : 0u;
+          vw[e] &= lo | hi;
+        }
+      }
+      *reinterpret_cast<u32x4 *>(&sK[buf * kBlockElems + k_lds(j * kPage + st_slot, st_kch)]) = kw;
+      *reinterpret_cast<u32x4 *>(&sV[buf * kBlockElems + v_lds(j, st_d, st_half)]) = vw;
     }
   };
 
-  // ---- per-lane operand addressing inside a block ----
-  // S tile t of pair pp, matrix row i = col holds key
-  //   32 pp + 16 (col >> 3) + 8 ((col >> 2) & 1) + 4 t + (col & 3).
-  const int ka_row = 16 * (col >> 3) + 8 * ((col >> 2) & 1) + (col & 3);  // + 32pp + 4t
-  const int ka_swz = k_swz(ka_row);
-  // S values / P^T / V^T operand of lane l: keys 32 pp + 16 (l >> 5) + 8 ((l >> 4) & 1) + e.
-  const int sv_page = lane >> 5, sv_half = (lane >> 4) & 1;
-  const int sv_key = 16 * sv_page + 8 * sv_half;                           // + 32pp + e
-  const int va_half = v_half(col, sv_half);      // (16 mt + col) >> 3 has the bit of col
+  // ---- operand addressing. A row i of an S tile holds key pi(i): bits 2 and
+  // 3 of i swapped, so that lane l's value r is key 16 (r / 8) + 8 grp + r % 8.
+  const int ka_key = (col & ~12) | ((col & 4) << 1) | ((col & 8) >> 1);
+  // With a positive scale the max is taken on raw scores and the scale is
+  // folded into the exponent's FMA; otherwise scores are scaled first.
+  const float c2 = a.scale_log2;
+  const float cs = kPosScale ? c2 : 1.f;
 
-  f32x4 o[8][kCols];
+  f32x16 o[4];
 #pragma unroll
-  for (int mt = 0; mt < 8; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < kCols; ++nt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[kCols], l_run[kCols];
-#pragma unroll
-  for (int nt = 0; nt < kCols; ++nt) {
-    m_run[nt] = -INFINITY;
-    l_run[nt] = 0.f;
-  }
+  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;   // running max (scaled, base 2) and sum
 
-  stage(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
+  stage_load(0);
+  stage_store(0, 0);
   __syncthreads();
 
   for (int blk = 0; blk < nblocks; ++blk) {
     const int buf = blk & 1;
-    if (blk + 1 < nblocks) stage(blk + 1, buf ^ 1);
-    const uint16_t *k_lds = sK[buf];
-    const uint16_t *v_lds = sV[buf];
-
+    if (blk + 1 < nblocks) stage_load(blk + 1);
+    const uint16_t *kl = sK + buf * kBlockElems;
+    const uint16_t *vl = sV + buf * kBlockElems;
     const int key0 = blk * kBlock;
     const bool need_mask = key0 + kBlock - 1 > wave_q0;
-    const bool tail = key0 + kBlock > row_end;
-    // The block is consumed one pair of pages (32 keys) at a time: scores,
-    // online-softmax update, then the P·V product of that pair.
+
+    // S^T of pair pp: 32 keys (pages 2pp, 2pp + 1 of the block) x 32 query rows.
+    auto scores = [&](int pp) __attribute__((always_inline)) {
+      // all eight K operands are requested before the first product
+      const int krow = 32 * pp + ka_key;
+      bf16x8 ka[8];
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp) {
-      f32x4 st[2][kCols];
+      for (int kk = 0; kk < 8; ++kk) ka[kk] = lds_bf16x8(&kl[k_lds(krow, 2 * kk + grp)]);
+      f32x16 st = f32x16{};
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int kk = 0; kk < 8; ++kk) st = mfma32x32x16(ka[kk], qop[kk], st);
+      return st;
+    };
+    // Online-softmax update and P·V of pair pp.
+    auto update = [&](int pp, f32x16 st) __attribute__((always_inline)) {
+      // V operands are requested first; their latency hides behind the softmax.
+      bf16x8 va[8];
 #pragma unroll
-        for (int nt = 0; nt < kCols; ++nt) st[t][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const int row = 32 * pp + 4 * t + ka_row;
+      for (int dt = 0; dt < 4; ++dt) {
+        va[2 * dt] = lds_bf16x8(&vl[v_lds(2 * pp, 32 * dt + col, grp)]);
+        va[2 * dt + 1] = lds_bf16x8(&vl[v_lds(2 * pp + 1, 32 * dt + col, grp)]);
+      }
+      float sc[16];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const bf16x8 ka = __builtin_bit_cast(
-              bf16x8, *reinterpret_cast<const u32x4 *>(
-                          &k_lds[row * kHeadDim + (((4 * kk + kgrp) ^ ka_swz) * 8)]));
+      for (int r = 0; r < 16; ++r) sc[r] = kPosScale ? st[r] : st[r] * c2;
+      if (need_mask) {
 #pragma unroll
-          for (int nt = 0; nt < kCols; ++nt) st[t][nt] = mfma16x16x32(ka, qop[nt][kk], st[t][nt]);
+        for (int r = 0; r < 16; ++r) {
+          const int kpos = key0 + 32 * pp + 16 * (r >> 3) + 8 * grp + (r & 7);
+          sc[r] = kpos > qpos ? -INFINITY : sc[r];
         }
       }
-
-      bf16x8 pb[kCols];
+      float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
 #pragma unroll
-      for (int nt = 0; nt < kCols; ++nt) {
-        float sc[8];
+      for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
+      mx = fmaxf(mx, sc[15]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      if (kPosScale) mx *= c2;
+      // Lazy rescaling: the running max only moves (and O, l are rescaled)
+      // when a score exceeds it by more than 2^kSlack; otherwise the stale
+      // max is kept and weights may reach 2^kSlack, which fp32 and bf16 carry
+      // without loss. out = O / l does not depend on the choice.
+      const bool grow = mx > m_run + kSlack;
+      if (__any(grow)) {
+        const float m_new = grow ? mx : m_run;
+        const float alpha = grow ? fast_exp2(m_run - m_new) : 1.f;
+        m_run = m_new;
+        l_run *= alpha;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sc[4 * t + r] = st[t][nt][r] * a.scale_log2;
-        if (need_mask) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int kpos = key0 + 32 * pp + sv_key + e;
-            sc[e] = kpos > qpos[nt] ? -INFINITY : sc[e];
-          }
-        }
-        float mx = sc[0];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sc[e]);
-        mx = col_max4(mx);
-        // Lazy rescaling: the running max only moves (and O, l are rescaled)
-        // when a score exceeds it by more than 2^kSlack; otherwise the stale
-        // max is kept and the weights may reach 2^kSlack, which fp32 and
-        // bf16 carry without loss. out = O / l does not depend on the choice.
-        const bool grow = mx > m_run[nt] + kSlack;
-        if (__any(grow)) {
-          const float m_new = grow ? mx : m_run[nt];
-          const float alpha = grow ? fast_exp2(m_run[nt] - m_new) : 1.f;
-          m_run[nt] = m_new;
-          l_run[nt] *= alpha;
-#pragma unroll
-          for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha;
-        }
-        const float m_use = m_run[nt] == -INFINITY ? 0.f : m_run[nt];
-        float psum = 0.f;
-        f32x8 p;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          p[e] = fast_exp2(sc[e] - m_use);
-          psum += p[e];
-        }
-        pb[nt] = to_bf16x8(p);
-        l_run[nt] += psum;
+        for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
       }
-
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      f32x8 p0, p1;
 #pragma unroll
-      for (int mt = 0; mt < 8; ++mt) {
-        const int d = 16 * mt + col;
-        bf16x8 va = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4 *>(
-                        &v_lds[((2 * pp + sv_page) * kHeadDim + d) * kPage + va_half * 8]));
-        if (tail) {
-          // keys at or past the row's end: replace (not multiply) by zero
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            va[e] = key0 + 32 * pp + sv_key + e >= row_end ? (__bf16)0.f : va[e];
-        }
-#pragma unroll
-        for (int nt = 0; nt < kCols; ++nt) o[mt][nt] = mfma16x16x32(va, pb[nt], o[mt][nt]);
+      for (int e = 0; e < 8; ++e) {
+        p0[e] = fast_exp2(__builtin_fmaf(sc[e], cs, -m_use));
+        p1[e] = fast_exp2(__builtin_fmaf(sc[8 + e], cs, -m_use));
       }
-    }
+      l_run += (((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]))) +
+               (((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7])));
+      const bf16x8 pb0 = to_bf16x8(p0), pb1 = to_bf16x8(p1);
+      // O^T[d][qrow] += V^T[d][key] P^T[key][qrow]: page c of the pair, slots
+      // 8 grp + 0..7, d = 32 dt + col.
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        o[dt] = mfma32x32x16(va[2 * dt], pb0, o[dt]);
+        o[dt] = mfma32x32x16(va[2 * dt + 1], pb1, o[dt]);
+      }
+    };
+    // The scores of the next pair are issued before the softmax of the
+    // current one, so the matrix cores work while the vector unit does.
+#pragma unroll
+    for (int pp = 0; pp < kBlock / 32; ++pp) update(pp, scores(pp));
 
-    __builtin_amdgcn_s_waitcnt(0);
+    if (blk + 1 < nblocks) stage_store(blk + 1, buf ^ 1);
     __syncthreads();
   }
 
-  // ---- epilogue: normalise and store (lane holds d = 16 mt + 4 kgrp + 0..3) ----
-#pragma unroll
-  for (int nt = 0; nt < kCols; ++nt) {
-    const float l = col_sum4(l_run[nt]);
-    if (qpos[nt] < 0) continue;
-    const int r = wave * kRowsPerWave + nt * 16 + col;
-    const int qi = r / G, hh = r - qi * G;
+  // ---- epilogue: normalise and store; lane holds d = 32 dt + 8 (r/4) + 4 grp + r%4 ----
+  const float l = l_run + __shfl_xor(l_run, 32);
+  if (qpos >= 0) {
     const size_t row = (size_t)(cu0 + i0 + qi) * a.hq + (size_t)g * G + hh;
     const float inv = 1.f / l;
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt)
-      *reinterpret_cast<f32x4 *>(&a.out[row * kHeadDim + 16 * mt + 4 * kgrp]) = o[mt][nt] * inv;
-    if (a.lse && kgrp == 0) a.lse[row] = (m_run[nt] + __log2f(l)) * kLn2;
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[dt][4 * rq + e] * inv;
+        *reinterpret_cast<f32x4 *>(&a.out[row * kHeadDim + 32 * dt + 8 * rq + 4 * grp]) = v;
+      }
+    if (a.lse && grp == 0) a.lse[row] = (m_run + __log2f(l)) * kLn2;
   }
 }
 
@@ -290,7 +301,11 @@ hipError_t launch_append(const uint16_t *q, const int32_t *cu_q, const int32_t *
   a.q_per_block = kRowsPerGroup / a.group;
   a.scale_log2 = scale * kLog2e;
   const int qblocks = (max_q_len + a.q_per_block - 1) / a.q_per_block;
-  hipLaunchKernelGGL(append_kernel, dim3(qblocks, kv.hkv, B), dim3(kThreads), 0, stream, a);
+  const dim3 grid(qblocks, kv.hkv, B);
+  if (a.scale_log2 > 0.f)
+    hipLaunchKernelGGL(append_kernel<true>, grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(append_kernel<false>, grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
