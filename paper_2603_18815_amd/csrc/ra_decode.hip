@@ -44,7 +44,10 @@ struct DecodeArgs {
 };
 
 __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a) {
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  // KV head fastest: the Hkv workgroups of one (row, split) are dispatched
+  // together, so the Hkv adjacent 4 KiB blocks of every page they read are
+  // requested close in time (DRAM row locality).
+  const int g = blockIdx.x, split = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int L = min(a.kv_lens[b], a.max_kv_len);
@@ -229,14 +232,15 @@ __global__ __launch_bounds__(kHeadDim) void decode_combine_kernel(
 }  // namespace
 
 DecodePlan decode_plan(int32_t B, int32_t hkv, int32_t max_kv_len) {
-  // Aim for about 16 splits per (row, KV head) slot of a full machine:
-  // enough workgroups to balance rows of different lengths, few enough that
-  // the partial results stay about 1 % of the KV bytes. Split boundaries are
-  // multiples of 128 keys (4 waves x one page pair) and depend only on the
-  // host-side sizes, never on page ids.
+  // Aim for about 8k (row, KV head, split) items on the longest-row bound:
+  // enough workgroups to balance rows of different lengths over 256 CUs,
+  // long enough splits that the partial results stay well under 1 % of the
+  // KV bytes. Split lengths are powers of two in [512, 4096] keys, multiples
+  // of 128 keys (4 waves x one page pair), and depend only on the host-side
+  // sizes, never on page ids.
   int64_t work = (int64_t)B * hkv * (int64_t)(max_kv_len > 0 ? max_kv_len : 1);
   int64_t split = 512;
-  while (split < 4096 && work / split > 16384) split *= 2;
+  while (split < 4096 && work / split > 8192) split *= 2;
   if (const char *env = getenv("RA_SPLIT_TOKENS")) {
     const long v = strtol(env, nullptr, 10);
     if (v >= 128) split = (v + 127) / 128 * 128;
@@ -275,7 +279,7 @@ hipError_t launch_decode(const uint16_t *q, const PagedKV &kv, const int32_t *kv
   a.split_tokens = plan.split_tokens;
   a.max_splits = plan.max_splits;
   a.scale_log2 = scale * kLog2e;
-  hipLaunchKernelGGL(decode_split_kernel, dim3(plan.max_splits, kv.hkv, B), dim3(kThreads), 0,
+  hipLaunchKernelGGL(decode_split_kernel, dim3(kv.hkv, plan.max_splits, B), dim3(kThreads), 0,
                      stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
