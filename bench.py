@@ -53,6 +53,37 @@ def write_bytes(n_new: int, Hkv: int, D: int = 128) -> int:
     return 2 * n_new * Hkv * D * 2 * 2
 
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCES = {
+    "decode": ("paper_2603_18815_amd/csrc/ra_decode.hip", "paper_2603_18815_amd/csrc/ra_device.h"),
+    "append": ("paper_2603_18815_amd/csrc/ra_append.hip", "paper_2603_18815_amd/csrc/ra_device.h"),
+}
+TRAFFIC_FILES = {
+    "decode": "profiles/decode_qwen3_8b_b64.hbm_traffic.txt",
+    "append": "profiles/append_qwen3_8b_b32.hbm_traffic.txt",
+}
+
+
+def measured_traffic(part: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    when there is none or the kernel source has changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, TRAFFIC_FILES[part])
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("#")[0].split("=", 1)
+            fields[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[part]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if fields.get("source_sha256_16") != h.hexdigest()[:16]:
+        return None
+    return int(float(fields["hbm_bytes_per_launch"]))
+
+
 def cpu_baseline(wd, td, wa, ta, seconds: float):
     """Time the fp64 oracle on bounded samples of the benchmark's own inputs."""
     import oracle
@@ -81,24 +112,28 @@ def cpu_baseline(wd, td, wa, ta, seconds: float):
     dec = {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
            "sample": f"decode, {rows_done} of {wd.kv_lens.shape[0]} rows of the decode "
                      f"workload (all heads), {spent:.1f} s wall"}
-    # append: single queries (query i of a row == a one-token chunk at ctx + i)
+    # append: single queries (query i of a row == a one-token chunk at ctx + i),
+    # drawn in batches of 64 from random rows until the time budget is spent
     cu = wa.cu_q()
-    qs, ctx1, rows = [], [], []
-    for r in rng.permutation(wa.q_lens.shape[0])[:4]:
-        for i in rng.integers(0, int(wa.q_lens[r]), 8):
-            qs.append(int(cu[r]) + int(i))
-            ctx1.append(int(wa.ctx_lens[r]) + int(i))
+    spent_a, flops, nq = 0.0, 0, 0
+    while spent_a < seconds and nq < 4096:
+        qs, ctx1, rows = [], [], []
+        for r in rng.integers(0, wa.q_lens.shape[0], 64):
+            i = int(rng.integers(0, int(wa.q_lens[r])))
+            qs.append(int(cu[r]) + i)
+            ctx1.append(int(wa.ctx_lens[r]) + i)
             rows.append(int(r))
-    ctx1 = np.array(ctx1, np.int32)
-    k, v, bt = compact_rows(ta.k_pool, ta.v_pool, wa.append_table()[np.array(rows)], ctx1 + 1)
-    q = bits(ta.q_append[torch.as_tensor(qs, device=dev)])
-    t0 = time.perf_counter()
-    oracle.append(q, np.arange(len(qs) + 1, dtype=np.int32), ctx1, k, v, bt, SCALE)
-    spent_a = time.perf_counter() - t0
-    flops = 4 * 128 * wa.Hq * int((ctx1.astype(np.int64) + 1).sum())
+        ctx1 = np.array(ctx1, np.int32)
+        k, v, bt = compact_rows(ta.k_pool, ta.v_pool, wa.append_table()[np.array(rows)], ctx1 + 1)
+        q = bits(ta.q_append[torch.as_tensor(qs, device=dev)])
+        t0 = time.perf_counter()
+        oracle.append(q, np.arange(len(qs) + 1, dtype=np.int32), ctx1, k, v, bt, SCALE)
+        spent_a += time.perf_counter() - t0
+        flops += 4 * 128 * wa.Hq * int((ctx1.astype(np.int64) + 1).sum())
+        nq += len(qs)
     app = {"value": flops / spent_a / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-           "sample": f"append, {len(qs)} single queries (all heads) from 4 rows of the append "
-                     f"workload, {spent_a:.2f} s wall"}
+           "sample": f"append, {nq} single queries (all heads) drawn from random rows of the "
+                     f"append workload, {spent_a:.1f} s wall"}
     return dec, app
 
 
@@ -108,8 +143,12 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
-                    help="budget of the decode leg of the CPU oracle baseline")
+                    help="time budget of each leg (decode, append) of the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["write", "decode", "append", "copy"],
+                    help="run only this part of the step --steps times after --warmup "
+                         "(for rocprofv3 counter runs; 'copy' is a 1 GiB torch copy used to "
+                         "calibrate the HBM byte counters); prints no JSON line")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -162,6 +201,27 @@ def main():
         ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a)
         if ev is not None:
             ev[3].record()
+
+    if args.only:
+        if args.only == "copy":
+            src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+            dst = torch.empty_like(src)
+            src.fill_(1)
+            part = lambda: dst.copy_(src)
+        else:
+            part = {"write": lambda: (ra.kv_page_write(td.k_new, td.v_new, cu_d_t, st_d_t, kv_dw,
+                                                       max_new_d, max_pos_d),
+                                      ra.kv_page_write(ta.k_new, ta.v_new, cu_a_t, st_a_t, kv_aw,
+                                                       max_new_a, max_pos_a)),
+                    "decode": lambda: ra.decode(td.q_decode, kv_d, kv_lens, max_kv_d, SCALE,
+                                                out=out_d, workspace=ws),
+                    "append": lambda: ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv_a,
+                                                SCALE, out=out_a)}[args.only]
+        for _ in range(args.warmup + args.steps):
+            part()
+        torch.cuda.synchronize()
+        print(f"[bench] ran {args.only} {args.warmup} + {args.steps} times", flush=True)
+        return
 
     for _ in range(args.warmup):
         step()
@@ -224,11 +284,12 @@ def main():
                        "GB_s": round(wbytes / (w_ms.mean() * 1e-3) / 1e9, 1)},
         "roofline": {"kernel": "rollout_attn_decode (decode_split_kernel + decode_combine_kernel)",
                      "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+                     "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("decode")},
         "roofline_append": {"kernel": "append_kernel", "bound": "mfma",
                             "achieved": round(app_tfs, 1), "peak": BF16_PEAK_TFLOPS,
                             "unit": "TFLOP/s", "frac": round(app_tfs / BF16_PEAK_TFLOPS, 4),
-                            "traffic": None},
+                            "traffic": measured_traffic("append")},
         "cpu_baseline": cpu_dec,
         "cpu_baseline_append": cpu_app,
     }
