@@ -15,9 +15,12 @@
 // receives are, in order, 8 consecutive slots of the first page and the same
 // 8 slots of the second: exactly the P^T operands of the two P·V products it
 // takes part in (no shuffles). Each query row stays in one lane column (two
-// lanes), so the online-softmax state is lane-local and the column max needs
-// a single cross-lane exchange. The causal mask (key position > ctx + i) is
-// applied only on blocks that reach past the wave's first query position.
+// lanes), so the online-softmax state is lane-local. Weights are taken
+// against a running max that moves only when they would grow too large
+// (a per-wave check on the weight sums), so the common path has no max
+// reduction and no cross-lane exchange. The causal mask (key position >
+// ctx + i) is applied only on blocks that reach past the wave's first query
+// position.
 #include "ra_device.h"
 #include "ra_internal.h"
 
@@ -35,7 +38,7 @@ constexpr int kBlockPages = kBlock / kPage;            // 4
 constexpr int kPagesPerPass = kThreads / 256;          // pages one staging pass covers
 constexpr int kPasses = kBlockPages / kPagesPerPass;   // 2
 constexpr int kBlockElems = kBlock * kHeadDim;         // per pool, per buffer
-constexpr float kSlack = 8.f;                          // lazy-rescale threshold (base 2)
+constexpr float kSumLimit = 16384.f;                  // weight-sum bound between rescales
 
 struct AppendArgs {
   const uint16_t *q;
@@ -57,18 +60,27 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Max of x over lanes l and l ^ 32 (one v_permlane32_swap: each lane gets
+// both values of its pair, in some order).
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 __device__ __forceinline__ bf16x8 lds_bf16x8(const uint16_t *p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
 }
 
-// LDS layouts (per buffer). K: 64 key rows x 128 dims (256 B rows); the
-// 16-byte chunk c of row R sits at chunk c ^ (R & 15), so the 16 rows that
-// one quarter-wave reads fall on distinct banks. V: [page][d][16 slots]
-// (32 B rows); the two 8-slot halves of row d are swapped when bit 3 of d is
-// set, for the same reason.
-__device__ __forceinline__ int k_lds(int row, int chunk) {
-  return row * kHeadDim + ((chunk ^ (row & 15)) * 8);
-}
+// LDS layouts (per buffer). K: 64 key rows x 128 dims, rows padded to
+// 272 B, so that 16 lanes reading the same chunk of 16 different rows (or 16
+// chunks of one row) fall on distinct banks, and a lane's eight operand reads
+// are one base address plus immediate offsets. V: [page][d][16 slots] (32 B
+// rows); the two 8-slot halves of row d are swapped when bit 3 of d is set,
+// for the same reason.
+constexpr int kKPitch = kHeadDim + 8;                   // K row pitch (elements)
+constexpr int kKBlockElems = kBlock * kKPitch;          // K buffer (elements)
+__device__ __forceinline__ int k_lds(int row, int chunk) { return row * kKPitch + chunk * 8; }
 __device__ __forceinline__ int v_lds(int page, int d, int half) {
   return (page * kHeadDim + d) * kPage + ((half ^ ((d >> 3) & 1)) * 8);
 }
@@ -96,7 +108,7 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
   const int32_t *bt = a.block_table + (size_t)b * a.bt_stride;
   const size_t head_stride = (size_t)kPage * kHeadDim;
 
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2 * kBlockElems];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2 * kKBlockElems];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2 * kBlockElems];
 
   // ---- this lane's query row and Q^T operands (dims 16 kk + 8 grp + 0..7) ----
@@ -138,11 +150,14 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
     for (int p = 0; p < kPasses; ++p) {
       const int j = p * kPagesPerPass + st_page;        // page in the block
       const int pos0 = (blk * kBlockPages + j) * kPage;
-      // Slots at or past the row's end may hold anything: store zeros instead.
-      u32x4 kw = kreg[p], vw = vreg[p];
-      if (pos0 + st_slot >= row_end) kw = u32x4{0u, 0u, 0u, 0u};
-      const int vpos = pos0 + st_half * 8;
-      if (vpos + 8 > row_end) {
+      // V slots at or past the row's end may hold anything (NaN included):
+      // they are stored as zeros, so that a zero weight cannot meet a NaN in
+      // the P·V product. K slots there need nothing: every key at or past
+      // the row's end lies beyond the causal limit of every query, and its
+      // score is replaced by -inf (a select, not an arithmetic mask).
+      u32x4 vw = vreg[p];
+      if (pos0 + kPage > row_end) {
+        const int vpos = pos0 + st_half * 8;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const uint32_t lo = vpos + 2 * e < row_end ? 0xffffu : 0u;
@@ -150,7 +165,8 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
           vw[e] &= lo | hi;
         }
       }
-      *reinterpret_cast<u32x4 *>(&sK[buf * kBlockElems + k_lds(j * kPage + st_slot, st_kch)]) = kw;
+      *reinterpret_cast<u32x4 *>(&sK[buf * kKBlockElems + k_lds(j * kPage + st_slot, st_kch)]) =
+          kreg[p];
       *reinterpret_cast<u32x4 *>(&sV[buf * kBlockElems + v_lds(j, st_d, st_half)]) = vw;
     }
   };
@@ -158,8 +174,8 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
   // ---- operand addressing. A row i of an S tile holds key pi(i): bits 2 and
   // 3 of i swapped, so that lane l's value r is key 16 (r / 8) + 8 grp + r % 8.
   const int ka_key = (col & ~12) | ((col & 4) << 1) | ((col & 8) >> 1);
-  // With a positive scale the max is taken on raw scores and the scale is
-  // folded into the exponent's FMA; otherwise scores are scaled first.
+  // With a positive scale the scores stay raw and the scale is folded into
+  // the exponent's FMA; otherwise scores are scaled first.
   const float c2 = a.scale_log2;
   const float cs = kPosScale ? c2 : 1.f;
 
@@ -175,7 +191,7 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
   for (int blk = 0; blk < nblocks; ++blk) {
     const int buf = blk & 1;
     if (blk + 1 < nblocks) stage_load(blk + 1);
-    const uint16_t *kl = sK + buf * kBlockElems;
+    const uint16_t *kl = sK + buf * kKBlockElems;
     const uint16_t *vl = sV + buf * kBlockElems;
     const int key0 = blk * kBlock;
     const bool need_mask = key0 + kBlock - 1 > wave_q0;
@@ -205,40 +221,46 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) sc[r] = kPosScale ? st[r] : st[r] * c2;
       if (need_mask) {
+        // value r is key key0 + 32 pp + 8 grp + 16 (r / 8) + r % 8; masked past qpos
+        const int rel = qpos - key0 - 32 * pp - 8 * grp;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kpos = key0 + 32 * pp + 16 * (r >> 3) + 8 * grp + (r & 7);
-          sc[r] = kpos > qpos ? -INFINITY : sc[r];
-        }
+        for (int r = 0; r < 16; ++r) sc[r] = 16 * (r >> 3) + (r & 7) > rel ? -INFINITY : sc[r];
       }
-      float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+      // Weights against the running max m_run. It is only moved (and O, l
+      // rescaled) when some lane's weights sum past kSumLimit, or are not
+      // finite (the first pair, while m_run is still -inf); the weights are
+      // then recomputed against the new max. Between moves every weight
+      // stays below kSumLimit, which fp32 and bf16 carry without loss, and
+      // out = O / l does not depend on when the max moves.
+      f32x8 p0, p1;
+      float psum;
+      auto weights = [&]() __attribute__((always_inline)) {
 #pragma unroll
-      for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
-      mx = fmaxf(mx, sc[15]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      if (kPosScale) mx *= c2;
-      // Lazy rescaling: the running max only moves (and O, l are rescaled)
-      // when a score exceeds it by more than 2^kSlack; otherwise the stale
-      // max is kept and weights may reach 2^kSlack, which fp32 and bf16 carry
-      // without loss. out = O / l does not depend on the choice.
-      const bool grow = mx > m_run + kSlack;
-      if (__any(grow)) {
-        const float m_new = grow ? mx : m_run;
-        const float alpha = grow ? fast_exp2(m_run - m_new) : 1.f;
+        for (int e = 0; e < 8; ++e) {
+          p0[e] = fast_exp2(__builtin_fmaf(sc[e], cs, -m_run));
+          p1[e] = fast_exp2(__builtin_fmaf(sc[8 + e], cs, -m_run));
+        }
+        psum = (((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]))) +
+               (((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7])));
+      };
+      weights();
+      if (!__all(psum <= kSumLimit)) {
+        float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+#pragma unroll
+        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
+        mx = fmaxf(mx, sc[15]);
+        mx = pair_max(mx);
+        if (kPosScale) mx *= c2;
+        float m_new = fmaxf(m_run, mx);
+        if (m_new == -INFINITY) m_new = 0.f;   // nothing attended yet: any finite reference
+        const float alpha = fast_exp2(m_run - m_new);
         m_run = m_new;
         l_run *= alpha;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
+        weights();
       }
-      const float m_use = m_run == -INFINITY ? 0.f : m_run;
-      f32x8 p0, p1;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p0[e] = fast_exp2(__builtin_fmaf(sc[e], cs, -m_use));
-        p1[e] = fast_exp2(__builtin_fmaf(sc[8 + e], cs, -m_use));
-      }
-      l_run += (((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]))) +
-               (((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7])));
+      l_run += psum;
       const bf16x8 pb0 = to_bf16x8(p0), pb1 = to_bf16x8(p1);
       // O^T[d][qrow] += V^T[d][key] P^T[key][qrow]: page c of the pair, slots
       // 8 grp + 0..7, d = 32 dt + col.
@@ -248,8 +270,6 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
         o[dt] = mfma32x32x16(va[2 * dt + 1], pb1, o[dt]);
       }
     };
-    // The scores of the next pair are issued before the softmax of the
-    // current one, so the matrix cores work while the vector unit does.
 #pragma unroll
     for (int pp = 0; pp < kBlock / 32; ++pp) update(pp, scores(pp));
 
