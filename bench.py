@@ -19,6 +19,9 @@ divided by the decode call's time); the append's algorithmic TFLOP/s (only
 unmasked query-key pairs, two matrix products each) is reported beside it.
 `roofline` is the decode kernel pair against the 8 TB/s HBM peak,
 `roofline_append` the append kernel against the 2.5 PFLOP/s dense bf16 peak.
+`mixed_step` times the mixed rollout step on one pool (B = 512 trajectories,
+85 % decode rows / 15 % append rows, log-normal contexts: page write, decode,
+append on one stream) beside its lower bounds at the published peaks.
 `cpu_baseline` is the fp64 CPU oracle on a bounded sample of the same inputs.
 """
 import argparse
@@ -137,6 +140,80 @@ def cpu_baseline(wd, td, wa, ta, seconds: float):
     return dec, app
 
 
+def mixed_step(ra, synth, dev, steps: int, warmup: int):
+    """Time the mixed rollout step of one pool: page write of the step's new
+    tokens, decode of the decode rows, append of the append rows (85 % / 15 %
+    of B = 512 trajectories, log-normal contexts), on one stream."""
+    import torch
+
+    w = synth.config(5)
+    t = synth.make_tensors(w, dev)
+
+    def i32(x):
+        return torch.as_tensor(np.ascontiguousarray(np.asarray(x, np.int32)), device=dev)
+
+    bt, cu, start = synth.write_plan(w)
+    kv_w = ra.PagedKV(t.k_pool, t.v_pool, i32(bt))
+    kv_d = kv_w.with_table(i32(w.decode_table()))
+    kv_a = kv_w.with_table(i32(w.append_table()))
+    cu_t, start_t = i32(cu), i32(start)
+    kv_lens, cu_q, ctx = i32(w.kv_lens), i32(w.cu_q()), i32(w.ctx_lens)
+    max_kv_d = int(w.kv_lens.max())
+    max_q, max_kv_a = int(w.q_lens.max()), int((w.ctx_lens + w.q_lens).max())
+    max_new = int(np.diff(cu).max())
+    max_pos = int(max(max_kv_d, max_kv_a))
+    out_d = torch.empty((w.kv_lens.shape[0], w.Hq, 128), dtype=torch.float32, device=dev)
+    out_a = torch.empty((int(w.q_lens.sum()), w.Hq, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty(ra.decode_workspace_size(w.kv_lens.shape[0], w.Hq, w.Hkv, max_kv_d),
+                     dtype=torch.uint8, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        ra.kv_page_write(t.k_new, t.v_new, cu_t, start_t, kv_w, max_new, max_pos)
+        if ev is not None:
+            ev[1].record()
+        ra.decode(t.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
+        if ev is not None:
+            ev[2].record()
+        ra.append(t.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for k in range(steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    w_ms = np.mean([e[0].elapsed_time(e[1]) for e in events])
+    d_ms = np.mean([e[1].elapsed_time(e[2]) for e in events])
+    a_ms = np.mean([e[2].elapsed_time(e[3]) for e in events])
+    s_ms = np.mean([e[0].elapsed_time(e[3]) for e in events])
+    dbytes, aflops = decode_bytes(w), append_flops(w)
+    wbytes = write_bytes(int(cu[-1]), w.Hkv)
+    # lower bounds at the published peaks: parts in sequence, and perfect overlap
+    kv_bytes_app = int((w.ctx_lens.astype(np.int64) + w.q_lens).sum()) * w.Hkv * 128 * 4
+    seq_ms = (dbytes + wbytes) / (HBM_PEAK_GBS * 1e6) + aflops / (BF16_PEAK_TFLOPS * 1e9)
+    ovl_ms = max((dbytes + wbytes + kv_bytes_app) / (HBM_PEAK_GBS * 1e6),
+                 aflops / (BF16_PEAK_TFLOPS * 1e9))
+    res = {
+        "workload": w.name, "steps": steps, "warmup": warmup,
+        "decode_rows": int(w.kv_lens.shape[0]), "append_rows": int(w.q_lens.shape[0]),
+        "ms": round(float(s_ms), 4), "page_write_ms": round(float(w_ms), 4),
+        "decode_ms": round(float(d_ms), 4), "append_ms": round(float(a_ms), 4),
+        "decode_algorithmic_bytes": dbytes, "append_algorithmic_flops": aflops,
+        "decode_GB_s": round(dbytes / (d_ms * 1e-3) / 1e9, 1),
+        "append_TFLOP_s": round(aflops / (a_ms * 1e-3) / 1e12, 1),
+        "bound_sequential_ms": round(seq_ms, 3), "bound_overlap_ms": round(ovl_ms, 3),
+        "frac_of_sequential_bound": round(seq_ms / s_ms, 4),
+    }
+    del t, out_d, out_a, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -145,6 +222,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="time budget of each leg (decode, append) of the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-mixed", action="store_true",
+                    help="skip the mixed-step leg (B = 512, 85 %% decode / 15 %% append rows)")
     ap.add_argument("--only", choices=["write", "decode", "append", "copy"],
                     help="run only this part of the step --steps times after --warmup "
                          "(for rocprofv3 counter runs; 'copy' is a 1 GiB torch copy used to "
@@ -244,6 +323,10 @@ def main():
     dec_gbs = dbytes / (d_ms.mean() * 1e-3) / 1e9
     app_tfs = aflops / (a_ms.mean() * 1e-3) / 1e12
 
+    mixed = None
+    if not args.no_mixed:
+        mixed = mixed_step(ra, synth, dev, min(args.steps, 10), min(args.warmup, 2))
+
     cpu_dec = cpu_app = None
     if not args.no_cpu_baseline:
         cpu_dec, cpu_app = cpu_baseline(wd, td, wa, ta, args.cpu_seconds)
@@ -290,6 +373,7 @@ def main():
                             "achieved": round(app_tfs, 1), "peak": BF16_PEAK_TFLOPS,
                             "unit": "TFLOP/s", "frac": round(app_tfs / BF16_PEAK_TFLOPS, 4),
                             "traffic": measured_traffic("append")},
+        "mixed_step": mixed,
         "cpu_baseline": cpu_dec,
         "cpu_baseline_append": cpu_app,
     }
