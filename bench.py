@@ -22,6 +22,8 @@ unmasked query-key pairs, two matrix products each) is reported beside it.
 `mixed_step` times the mixed rollout step on one pool (B = 512 trajectories,
 85 % decode rows / 15 % append rows, log-normal contexts: page write, decode,
 append on one stream) beside its lower bounds at the published peaks.
+`shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
+rollouts whose rows share each task's prompt pages.
 `cpu_baseline` is the fp64 CPU oracle on a bounded sample of the same inputs.
 """
 import argparse
@@ -214,6 +216,79 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
     return res
 
 
+def shared_prefix_bytes(w) -> int:
+    """Algorithmic bytes of shared-prefix decode: each group's shared keys once, each
+    row's other keys, q, out, its block-table entries and length."""
+    L = w.kv_lens.astype(np.int64)
+    D, P = w.head_dim, w.page_size
+    pre = np.repeat(w.prefix_len.astype(np.int64), np.diff(w.group_start))
+    per_row = ((L - pre) * w.Hkv * D * 4 + w.Hq * D * 2 + w.Hq * D * 4
+               + 4 * ((L + P - 1) // P) + 4)
+    return int(per_row.sum() + (w.prefix_len.astype(np.int64) * w.Hkv * D * 4).sum())
+
+
+def shared_prefix_leg(ra, synth, dev, steps: int, warmup: int):
+    """Plain decode vs shared-prefix decode of 8 tasks x 8 rollouts (rows of a task
+    share its prompt pages)."""
+    import torch
+
+    w = synth.config(6)
+    t = synth.make_tensors(w, dev)
+
+    def i32(x):
+        return torch.as_tensor(np.ascontiguousarray(np.asarray(x, np.int32)), device=dev)
+
+    kv = ra.PagedKV(t.k_pool, t.v_pool, i32(w.decode_table()))
+    lens, gs, pre = i32(w.kv_lens), i32(w.group_start), i32(w.prefix_len)
+    B, max_kv = w.kv_lens.shape[0], int(w.kv_lens.max())
+    mgr, mpl = int(np.diff(w.group_start).max()), int(w.prefix_len.max())
+    out = torch.empty((B, w.Hq, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty(ra.decode_shared_prefix_workspace_size(B, w.Hq, w.Hkv, max_kv, mpl),
+                     dtype=torch.uint8, device=dev)
+    # the same rows in an interleaved order (the rollouts of a task 8 rows apart, as
+    # requests arrive), for which the cache sees no reuse between a task's rows
+    n_g = w.group_start.size - 1
+    perm = np.arange(B).reshape(n_g, -1).T.reshape(-1)
+    kv_i = ra.PagedKV(t.k_pool, t.v_pool, i32(w.decode_table()[perm]))
+    q_i, lens_i = t.q_decode[torch.as_tensor(perm, device=dev)].contiguous(), i32(w.kv_lens[perm])
+    calls = {
+        "plain": lambda: ra.decode(t.q_decode, kv, lens, max_kv, SCALE, out=out, workspace=ws),
+        "plain_interleaved": lambda: ra.decode(q_i, kv_i, lens_i, max_kv, SCALE, out=out,
+                                               workspace=ws),
+        "shared": lambda: ra.decode_shared_prefix(t.q_decode, kv, lens, gs, pre, mgr, mpl,
+                                                  max_kv, SCALE, out=out, workspace=ws),
+    }
+    ms = {}
+    for name, fn in calls.items():
+        for _ in range(warmup):
+            fn()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for e in ev:
+            e[0].record()
+            fn()
+            e[1].record()
+        torch.cuda.synchronize()
+        ms[name] = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    plain_b, shared_b = decode_bytes(w), shared_prefix_bytes(w)
+    res = {
+        "workload": w.name, "steps": steps, "warmup": warmup,
+        "plain_ms": round(ms["plain"], 4),
+        "plain_interleaved_ms": round(ms["plain_interleaved"], 4),
+        "shared_ms": round(ms["shared"], 4),
+        "speedup_vs_plain": round(ms["plain"] / ms["shared"], 3),
+        "speedup_vs_plain_interleaved": round(ms["plain_interleaved"] / ms["shared"], 3),
+        "plain_algorithmic_bytes": plain_b, "shared_algorithmic_bytes": shared_b,
+        "plain_GB_s": round(plain_b / (ms["plain"] * 1e-3) / 1e9, 1),
+        "plain_interleaved_GB_s": round(plain_b / (ms["plain_interleaved"] * 1e-3) / 1e9, 1),
+        "shared_GB_s": round(shared_b / (ms["shared"] * 1e-3) / 1e9, 1),
+        "shared_frac_hbm_peak": round(shared_b / (ms["shared"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "shared_effective_GB_s": round(plain_b / (ms["shared"] * 1e-3) / 1e9, 1),
+    }
+    del t, out, ws, q_i
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -222,6 +297,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="time budget of each leg (decode, append) of the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-shared-prefix", action="store_true",
+                    help="skip the shared-prefix decode leg (8 tasks x 8 rollouts)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-step leg (B = 512, 85 %% decode / 15 %% append rows)")
     ap.add_argument("--only", choices=["write", "decode", "append", "copy"],
@@ -323,6 +400,9 @@ def main():
     dec_gbs = dbytes / (d_ms.mean() * 1e-3) / 1e9
     app_tfs = aflops / (a_ms.mean() * 1e-3) / 1e12
 
+    shared = None
+    if not args.no_shared_prefix:
+        shared = shared_prefix_leg(ra, synth, dev, args.steps, args.warmup)
     mixed = None
     if not args.no_mixed:
         mixed = mixed_step(ra, synth, dev, min(args.steps, 10), min(args.warmup, 2))
@@ -374,6 +454,7 @@ def main():
                             "unit": "TFLOP/s", "frac": round(app_tfs / BF16_PEAK_TFLOPS, 4),
                             "traffic": measured_traffic("append")},
         "mixed_step": mixed,
+        "shared_prefix_decode": shared,
         "cpu_baseline": cpu_dec,
         "cpu_baseline_append": cpu_app,
     }

@@ -123,6 +123,47 @@ int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_
                         void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Shared-prefix decode: decode for groups of rows whose caches begin with the
+ * same physical pages, e.g. the rollouts of one task, which share its prompt
+ * (Sec. 4 generates several rollouts per task instance; Sec. 3.3.2 keeps all
+ * calls of a task on one backend so that its cached prefix is reused). The
+ * result is that of rollout_attn_decode on the same rows (up to rounding: the
+ * keys are split differently); the shared keys are read once per group (per
+ * 32 / (Hq / Hkv) rows of a group) instead of once per row.
+ * For group i, rows group_start[i] .. group_start[i+1]-1 attend their first P_i
+ * keys together, P_i = min(prefix_len[i], shortest kv_lens of the group)
+ * rounded down to a multiple of 32, read through the block table of the
+ * group's first row; each row attends its keys P_i .. kv_lens[b]-1 alone.
+ *
+ *   q, kv, kv_lens, out, lse, scale: as rollout_attn_decode
+ *   group_start     int32 [num_groups + 1], group_start[0] = 0, non-decreasing,
+ *                   group_start[num_groups] = B (every row in one group)
+ *   prefix_len      int32 [num_groups]: positions [0, prefix_len[i]) of every
+ *                   row of group i map to the same pages as the group's first
+ *                   row (a precondition: not checked; violating it gives wrong
+ *                   numbers, never an out-of-bounds access)
+ *   max_group_rows  host: an upper bound of the rows of a group, <= B
+ *   max_prefix_len  host: an upper bound of prefix_len, <= max_kv_len
+ *   workspace       device scratch of at least
+ *                   rollout_attn_decode_shared_prefix_workspace_size(B, Hq, Hkv,
+ *                   max_kv_len, max_prefix_len) bytes (contents on entry ignored)
+ * Errors: as rollout_attn_decode; RA_ERR_SHAPE also for num_groups == 0 or
+ *         max_group_rows == 0 with B > 0, max_group_rows > B, num_groups > B,
+ *         max_prefix_len > max_kv_len; RA_ERR_UNSUPPORTED when num_groups *
+ *         max_group_rows (or the prefix grid) exceeds 65535.
+ */
+size_t rollout_attn_decode_shared_prefix_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
+                                                        int32_t max_kv_len,
+                                                        int32_t max_prefix_len);
+int rollout_attn_decode_shared_prefix(const void *q, const ra_paged_kv *kv,
+                                      const int32_t *kv_lens, const int32_t *group_start,
+                                      const int32_t *prefix_len, int32_t B, int32_t Hq,
+                                      int32_t num_groups, int32_t max_group_rows,
+                                      int32_t max_prefix_len, int32_t max_kv_len, float scale,
+                                      float *out, float *lse, void *workspace,
+                                      size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Append: causal chunked prefill of newly appended observation tokens against
  * each trajectory's cache (Sec. 3.3.3: earlier turns keep their tokens, new
  * observations are tokenised and appended). Row b owns packed queries

@@ -23,8 +23,9 @@ from ._lib import RolloutAttnError  # noqa: F401  (re-export)
 PAGE_SIZE = 16
 HEAD_DIM = 128
 
-__all__ = ["PagedKV", "decode", "append", "kv_page_write", "kv_page_gather",
-           "decode_workspace_size", "abi_version", "RolloutAttnError"]
+__all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "kv_page_write",
+           "kv_page_gather", "decode_workspace_size", "decode_shared_prefix_workspace_size",
+           "abi_version", "RolloutAttnError"]
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -129,6 +130,63 @@ def decode(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor, max_kv_len: Opti
     _lib.check("rollout_attn_decode", lib.rollout_attn_decode(
         q.data_ptr(), ctypes.byref(s), kv_lens.data_ptr(), B, Hq, max_kv_len, float(scale),
         out.data_ptr(), _ptr(lse), workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
+    return out, lse
+
+
+def decode_shared_prefix_workspace_size(B: int, Hq: int, Hkv: int, max_kv_len: int,
+                                        max_prefix_len: int) -> int:
+    return int(_lib.load().rollout_attn_decode_shared_prefix_workspace_size(
+        B, Hq, Hkv, max_kv_len, max_prefix_len))
+
+
+def decode_shared_prefix(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor,
+                         group_start: torch.Tensor, prefix_len: torch.Tensor,
+                         max_group_rows: int, max_prefix_len: int,
+                         max_kv_len: Optional[int] = None, scale: Optional[float] = None,
+                         out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                         want_lse: bool = False, workspace: Optional[torch.Tensor] = None,
+                         stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Decode for groups of rows that share their first prefix_len[i] cached tokens.
+
+    group_start int32 [G+1] (row offsets of the groups), prefix_len int32 [G];
+    the result equals decode() on the same rows up to rounding.
+    """
+    lib = _lib.load()
+    dev = kv.device
+    _need(q, "q", torch.bfloat16, dev)
+    _need(kv_lens, "kv_lens", torch.int32, dev)
+    _need(group_start, "group_start", torch.int32, dev)
+    _need(prefix_len, "prefix_len", torch.int32, dev)
+    B, Hq, D = q.shape
+    _shape(q, (B, Hq, HEAD_DIM), "q")
+    _shape(kv_lens, (B,), "kv_lens")
+    ng = prefix_len.shape[0]
+    _shape(group_start, (ng + 1,), "group_start")
+    _rows(kv, B)
+    if max_kv_len is None:
+        max_kv_len = int(kv_lens.max().item()) if B else 0
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, dev)
+    _shape(out, (B, Hq, HEAD_DIM), "out")
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+        _shape(lse, (B, Hq), "lse")
+    ws_bytes = lib.rollout_attn_decode_shared_prefix_workspace_size(
+        B, Hq, kv.num_kv_heads, max_kv_len, max_prefix_len)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    _need(workspace, "workspace", torch.uint8, dev)
+    s = kv.struct()
+    _lib.check("rollout_attn_decode_shared_prefix", lib.rollout_attn_decode_shared_prefix(
+        q.data_ptr(), ctypes.byref(s), kv_lens.data_ptr(), group_start.data_ptr(),
+        prefix_len.data_ptr(), B, Hq, ng, max_group_rows, max_prefix_len, max_kv_len,
+        float(scale), out.data_ptr(), _ptr(lse), workspace.data_ptr(), workspace.numel(),
+        _stream(dev, stream)))
     return out, lse
 
 

@@ -74,6 +74,46 @@ int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_
                                       stream));
 }
 
+size_t rollout_attn_decode_shared_prefix_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
+                                                        int32_t max_kv_len,
+                                                        int32_t max_prefix_len) {
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || max_kv_len < 0 || max_prefix_len < 0) return 0;
+  return ra::shared_prefix_workspace_bytes(B, Hq, ra::decode_plan(B, Hkv, max_kv_len),
+                                           max_prefix_len);
+}
+
+int rollout_attn_decode_shared_prefix(const void *q, const ra_paged_kv *kv,
+                                      const int32_t *kv_lens, const int32_t *group_start,
+                                      const int32_t *prefix_len, int32_t B, int32_t Hq,
+                                      int32_t num_groups, int32_t max_group_rows,
+                                      int32_t max_prefix_len, int32_t max_kv_len, float scale,
+                                      float *out, float *lse, void *workspace,
+                                      size_t workspace_bytes, hipStream_t stream) {
+  if (B < 0 || Hq <= 0 || max_kv_len < 0 || num_groups < 0 || max_group_rows < 0 ||
+      max_prefix_len < 0)
+    return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!q || !kv_lens || !out || !group_start || !prefix_len) return RA_ERR_NULL;
+  if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
+  if (Hq / kv->num_kv_heads > 16 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_kv_len) || max_prefix_len > max_kv_len) return RA_ERR_SHAPE;
+  if (B == 0) return RA_OK;
+  if (num_groups == 0 || max_group_rows == 0 || max_group_rows > B || num_groups > B)
+    return RA_ERR_SHAPE;
+  const ra::SharedPrefixShape sh =
+      ra::shared_prefix_shape(Hq / kv->num_kv_heads, num_groups, max_group_rows);
+  if (sh.prefix_z > kMaxGridYZ || sh.row_z > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  const ra::DecodePlan plan = ra::decode_plan(B, kv->num_kv_heads, max_kv_len);
+  if (!workspace ||
+      workspace_bytes < ra::shared_prefix_workspace_bytes(B, Hq, plan, max_prefix_len))
+    return RA_ERR_WORKSPACE;
+  return hip_status(ra::launch_decode_shared_prefix(
+      static_cast<const uint16_t *>(q), to_internal(kv), kv_lens, group_start, prefix_len, B, Hq,
+      num_groups, max_group_rows, max_prefix_len, max_kv_len, scale, out, lse, workspace, plan,
+      stream));
+}
+
 int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_lens,
                         const ra_paged_kv *kv, int32_t B, int32_t Hq, int32_t total_q,
                         int32_t max_q_len, int32_t max_kv_len, float scale, float *out,

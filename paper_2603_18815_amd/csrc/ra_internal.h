@@ -30,6 +30,25 @@ hipError_t launch_decode(const uint16_t *q, const PagedKV &kv, const int32_t *kv
                          int32_t hq, int32_t max_kv_len, float scale, float *out, float *lse,
                          void *workspace, const DecodePlan &plan, hipStream_t stream);
 
+// ---- shared-prefix decode (rows of a group share their first prefix pages) ----
+// Grid sizes of one call: a prefix workgroup covers rows_per_chunk rows of a
+// group (tiles 16-column tiles); prefix_z / row_z are the grid z extents.
+struct SharedPrefixShape {
+  int32_t rows_per_chunk, tiles, chunks;
+  int64_t prefix_z, row_z;
+};
+SharedPrefixShape shared_prefix_shape(int32_t group, int32_t num_groups, int32_t max_group_rows);
+int32_t prefix_slots(const DecodePlan &plan, int32_t max_prefix_len);
+size_t shared_prefix_workspace_bytes(int32_t B, int32_t hq, const DecodePlan &plan,
+                                     int32_t max_prefix_len);
+hipError_t launch_decode_shared_prefix(const uint16_t *q, const PagedKV &kv,
+                                       const int32_t *kv_lens, const int32_t *group_start,
+                                       const int32_t *prefix_len, int32_t B, int32_t hq,
+                                       int32_t num_groups, int32_t max_group_rows,
+                                       int32_t max_prefix_len, int32_t max_kv_len, float scale,
+                                       float *out, float *lse, void *workspace,
+                                       const DecodePlan &plan, hipStream_t stream);
+
 // ---- append (causal chunked prefill against the cache) ----
 hipError_t launch_append(const uint16_t *q, const int32_t *cu_q, const int32_t *ctx_lens,
                          const PagedKV &kv, int32_t B, int32_t hq, int32_t total_q,

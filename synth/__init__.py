@@ -61,6 +61,10 @@ class Workload:
     seed: int
     head_dim: int = HEAD_DIM
     page_size: int = PAGE
+    # shared-prefix decode: row offsets of the groups [G + 1] and the tokens
+    # the rows of each group share [G] (None for other workloads)
+    group_start: Optional[np.ndarray] = None
+    prefix_len: Optional[np.ndarray] = None
 
     @property
     def G(self) -> int:
@@ -110,6 +114,60 @@ def make_layout(rng: np.random.Generator, row_tokens, page_size: int = PAGE,
     return PagedLayout(num_pages, bt, row_tokens.astype(np.int32), decoys)
 
 
+def shared_prefix_layout(rng: np.random.Generator, group_sizes, prefix_tokens, suffix_tokens,
+                         page_size: int = PAGE, decoy_frac: float = 0.01,
+                         min_decoys: int = 16) -> PagedLayout:
+    """Rows in consecutive groups; the rows of group i share the pages of their
+    first prefix_tokens[i] tokens (a multiple of the page size), then each row
+    owns the pages of its suffix_tokens[r] further tokens. Page ids shuffled."""
+    sizes = np.asarray(group_sizes, np.int64)
+    pre = np.asarray(prefix_tokens, np.int64)
+    suf = np.asarray(suffix_tokens, np.int64)
+    assert np.all(pre % page_size == 0) and suf.shape[0] == sizes.sum()
+    row_group = np.repeat(np.arange(sizes.shape[0]), sizes)
+    pre_pages = pre // page_size
+    suf_pages = (suf + page_size - 1) // page_size
+    n_used = int(pre_pages.sum() + suf_pages.sum())
+    n_decoy = max(min_decoys, int(math.ceil(decoy_frac * n_used)))
+    num_pages = n_used + n_decoy
+    perm = rng.permutation(num_pages).astype(np.int32)
+    decoys = perm[n_used:]
+    row_pages = pre_pages[row_group] + suf_pages
+    stride = max(1, int(row_pages.max()))
+    B = suf.shape[0]
+    bt = np.empty((B, stride), np.int32)
+    off = 0
+    shared = []
+    for i in range(sizes.shape[0]):
+        shared.append(perm[off:off + int(pre_pages[i])])
+        off += int(pre_pages[i])
+    for b in range(B):
+        sp = shared[row_group[b]]
+        n = int(suf_pages[b])
+        bt[b, :sp.shape[0]] = sp
+        bt[b, sp.shape[0]:sp.shape[0] + n] = perm[off:off + n]
+        rest = stride - sp.shape[0] - n
+        if rest:
+            bt[b, stride - rest:] = decoys[(b + np.arange(rest)) % n_decoy]
+        off += n
+    return PagedLayout(num_pages, bt, (pre[row_group] + suf).astype(np.int32), decoys)
+
+
+def shared_prefix_workload(seed: int, n_groups: int, rows_per_group: int, Hq: int, Hkv: int,
+                           prefix, suffix, name: str) -> Workload:
+    """Decode rows in groups of rows_per_group that share a prefix (whole pages)."""
+    rng = np.random.default_rng(seed)
+    pre = np.asarray(prefix(rng, n_groups), np.int64) // PAGE * PAGE
+    B = n_groups * rows_per_group
+    suf = np.asarray(suffix(rng, B), np.int64)
+    lay = shared_prefix_layout(rng, [rows_per_group] * n_groups, pre, suf)
+    e = np.zeros(0, np.int32)
+    gs = (np.arange(n_groups + 1) * rows_per_group).astype(np.int32)
+    return Workload(name, Hq, Hkv, lay, np.arange(B, dtype=np.int32),
+                    lay.row_tokens.astype(np.int32), e, e, e, seed,
+                    group_start=gs, prefix_len=pre.astype(np.int32))
+
+
 # ---------------------------------------------------------------------------
 # The five rollout workloads (lengths in tokens, page size 16, head dim 128).
 # ---------------------------------------------------------------------------
@@ -149,7 +207,7 @@ def mixed_workload(seed: int, B: int, Hq: int, Hkv: int, append_frac: float, ctx
 
 
 def config(c: int) -> Workload:
-    """The five rollout-attention workloads, numbered 1..5."""
+    """The rollout-attention workloads, numbered 1..6 (6: shared-prefix decode)."""
     if c == 1:
         return decode_workload(1, 4, 8, 2, lambda r, n: uniform_int(r, n, 32, 256),
                                "decode B=4 Hq=8 Hkv=2 L~U[32,256]")
@@ -172,6 +230,13 @@ def config(c: int) -> Workload:
                               lambda r, n: uniform_int(r, n, 128, 4096),
                               "mixed B=512 Hq=32 Hkv=8 85% decode / 15% append "
                               "ctx~LN(12288,0.75)[512,65536] T~U[128,4096]")
+    if c == 6:
+        return shared_prefix_workload(6, 8, 8, 32, 8,
+                                      lambda r, n: uniform_int(r, n, 2048, 8192),
+                                      lambda r, n: uniform_int(r, n, 2048, 24576),
+                                      "decode shared prefix B=64 (8 tasks x 8 rollouts) "
+                                      "Hq=32 Hkv=8 prompt~U[2048,8192] "
+                                      "rollout~U[2048,24576]")
     raise ValueError(f"unknown workload {c}")
 
 

@@ -79,6 +79,36 @@ def test_decode_validation(lib):
     assert _decode(lib, _kv(), B=0) == _lib.RA_OK                         # no work, no launch
 
 
+def test_shared_prefix_decode_validation(lib):
+    def call(kv=None, **kw):
+        d = dict(q=FAKE, kv_lens=FAKE, gs=FAKE, pre=FAKE, B=16, Hq=4, ng=2, mgr=8, mpl=32,
+                 max_kv_len=64, out=FAKE, ws=FAKE, ws_bytes=1 << 30)
+        d.update(kw)
+        return lib.rollout_attn_decode_shared_prefix(
+            d["q"], ctypes.byref(kv if kv is not None else _kv()), d["kv_lens"], d["gs"],
+            d["pre"], d["B"], d["Hq"], d["ng"], d["mgr"], d["mpl"], d["max_kv_len"], 0.1,
+            d["out"], None, d["ws"], d["ws_bytes"], None)
+    assert call(gs=None) == _lib.RA_ERR_NULL
+    assert call(pre=None) == _lib.RA_ERR_NULL
+    assert call(ng=-1) == _lib.RA_ERR_SHAPE
+    assert call(ng=0) == _lib.RA_ERR_SHAPE           # rows must belong to groups
+    assert call(mgr=0) == _lib.RA_ERR_SHAPE
+    assert call(mgr=17) == _lib.RA_ERR_SHAPE         # more rows per group than rows
+    assert call(mpl=65) == _lib.RA_ERR_SHAPE         # prefix bound above max_kv_len
+    assert call(Hq=5) == _lib.RA_ERR_SHAPE
+    assert call(Hq=34) == _lib.RA_ERR_UNSUPPORTED    # group of 17 query heads
+    assert call(ws_bytes=16) == _lib.RA_ERR_WORKSPACE
+    assert call(ws=None) == _lib.RA_ERR_WORKSPACE
+    big = dict(B=65535, ng=65535, mgr=2, max_kv_len=64)
+    assert call(**big) == _lib.RA_ERR_UNSUPPORTED    # grid of groups x rows too large
+    assert call(B=0) == _lib.RA_OK
+    f = lib.rollout_attn_decode_shared_prefix_workspace_size
+    plain = lib.rollout_attn_decode_workspace_size(64, 32, 8, 32768)
+    assert f(64, 32, 8, 32768, 0) == plain           # no prefix slots
+    assert f(64, 32, 8, 32768, 8192) > plain         # plus the prefix slots
+    assert f(0, 32, 8, 32768, 8192) == 0
+
+
 def test_append_validation(lib):
     def call(kv, **kw):
         d = dict(q=FAKE, cu=FAKE, ctx=FAKE, B=2, Hq=4, total_q=10, max_q=5, max_kv=64,

@@ -67,3 +67,25 @@ def test_poison_marks_decoys_and_tails():
         assert not torch.isnan(t.k_pool[pg, :, (L - 1) % 16].float()).any()
         if L % 16:
             assert torch.isnan(t.k_pool[pg, :, L % 16:].float()).all()
+
+
+def test_shared_prefix_layout():
+    w = synth.config(6)
+    lay, P = w.layout, w.page_size
+    assert w.group_start.tolist() == list(range(0, 65, 8)) and w.G == 4
+    assert np.all(w.prefix_len % P == 0) and w.prefix_len.min() >= 2048
+    assert np.all(w.kv_lens - np.repeat(w.prefix_len, 8) >= 2048)
+    owned = []
+    for i in range(w.prefix_len.size):
+        rows = range(w.group_start[i], w.group_start[i + 1])
+        n = w.prefix_len[i] // P
+        shared = lay.block_table[rows[0], :n]
+        for r in rows:       # every row of a group maps its prefix to the same pages
+            np.testing.assert_array_equal(lay.block_table[r, :n], shared)
+            owned.append(lay.block_table[r, n:(w.kv_lens[r] + P - 1) // P])
+        owned.append(shared)
+    owned = np.concatenate(owned)
+    # shared pages once per group, suffix pages once per row, decoys never owned
+    assert len(np.unique(owned)) == owned.size
+    assert np.intersect1d(owned, lay.decoys).size == 0
+    assert owned.size + lay.decoys.size == lay.num_pages
