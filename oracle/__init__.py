@@ -4,8 +4,8 @@ Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
 import this package. It shares no code with the HIP library
 (`paper_2603_18815_amd`) and never imports it.
 
-The arithmetic lives in `attn_oracle.c` (plain loops, fp64, libm exp/log); this
-module only marshals numpy arrays into it. What each function computes and the
+The arithmetic lives in `attn_oracle.c` and `logprob_oracle.c` (plain loops,
+fp64, libm exp/log); this module only marshals numpy arrays into it. What each function computes and the
 readings it adopts where the paper is silent are stated at the top of that file.
 Every function here is pinned by the `-m "not gpu"` tests in
 `tests/test_oracle_pins.py` (library routine, closed forms, invariants, brute
@@ -29,8 +29,8 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_build.LIB) or (
-        os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC)
+    if not os.path.exists(_build.LIB) or any(
+        os.path.getmtime(_build.LIB) < os.path.getmtime(src) for src in _build.SRCS
     ):
         _build.build()
     lib = ctypes.CDLL(_build.LIB)
@@ -47,6 +47,9 @@ def _load():
     lib.oracle_page_gather.argtypes = [_u16p, _u16p, _i32p, c_i64, _i32p, _i32p, c_int, c_int,
                                        c_int, c_int, _u16p, _u16p]
     lib.oracle_page_gather.restype = c_int
+    lib.oracle_token_logprob_f64.argtypes = [_u16p, _u16p, _i32p, c_i64, c_i64, c_i64, c_dbl,
+                                             _f64p, _f64p]
+    lib.oracle_token_logprob_f64.restype = c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = c_int
     _lib = lib
@@ -155,3 +158,22 @@ def page_gather(k_pool, v_pool, block_table, lens, cu_out):
     if rc != 0:
         raise RuntimeError(f"oracle_page_gather failed ({rc})")
     return k_out, v_out
+
+
+def token_logprob(h, W, targets, scale=1.0):
+    """Per-token log-probability of targets[n] under logits scale * h[n] . W^T.
+
+    h: uint16 bf16 bits [N][D]; W: uint16 bf16 bits [V][D]; targets: int [N].
+    Returns (logp [N], lse [N]) in fp64; logp is NaN for a target outside [0, V).
+    """
+    h = np.ascontiguousarray(h, np.uint16)
+    W = np.ascontiguousarray(W, np.uint16)
+    t = np.ascontiguousarray(targets, np.int32)
+    N, D = h.shape
+    V = W.shape[0]
+    assert W.shape[1] == D and t.shape == (N,)
+    logp = np.empty(N, np.float64)
+    lse = np.empty(N, np.float64)
+    rc = _load().oracle_token_logprob_f64(h, W, t, N, V, D, float(scale), logp, lse)
+    assert rc == 0
+    return logp, lse

@@ -353,3 +353,73 @@ def test_gather_matches_subscript_reading():
         np.testing.assert_array_equal(ko[cu[b]:cu[b + 1]], kd[b].transpose(1, 0, 2))
         np.testing.assert_array_equal(vo[cu[b]:cu[b + 1]], vd[b].transpose(1, 0, 2))
         np.testing.assert_array_equal(kd[b], ks[b])
+
+
+# ----------------------------------------------------------------------------- token log-probs
+
+def _golden(name):
+    vals = {}
+    for line in open(os.path.join(GOLDEN, name)):
+        if line.strip() and not line.startswith("#"):
+            k, v = line.split()
+            vals[k] = float(v)
+    return vals
+
+
+def test_logprob_matches_library_log_softmax():
+    """numpy fp64 matmul + scipy's log_softmax (an independent implementation)."""
+    from scipy.special import log_softmax
+    rng = np.random.default_rng(71)
+    N, V, D = 5, 37, 48
+    h, W = randn_bits(rng, (N, D)), randn_bits(rng, (V, D))
+    t = np.array([0, 36, 5, 17, 5], np.int32)
+    for scale in (1.0, 0.7):
+        z = scale * (bits_f64(h) @ bits_f64(W).T)          # [N][V]
+        ref = log_softmax(z, axis=1)
+        logp, lse = oracle.token_logprob(h, W, t, scale)
+        np.testing.assert_allclose(logp, ref[np.arange(N), t], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse, z[np.arange(N), t] - ref[np.arange(N), t], rtol=1e-13)
+
+
+def test_logprob_golden_three_tokens():
+    g = _golden("logprob_three_tokens.txt")
+    h = bf16_bits([[1.0, 0.0]] * 3)
+    W = bf16_bits([[0.0, 0.0], [1.0, 0.0], [2.0, 0.0]])
+    logp, lse = oracle.token_logprob(h, W, [0, 1, 2])
+    for i in range(3):
+        assert abs(logp[i] - g[f"logp{i}"]) < 1e-14
+        assert abs(lse[i] - g["lse"]) < 1e-14
+
+
+def test_logprob_closed_forms():
+    rng = np.random.default_rng(72)
+    V, D = 29, 32
+    W = randn_bits(rng, (V, D))
+    # zero hidden state: uniform distribution
+    logp, lse = oracle.token_logprob(np.zeros((2, D), np.uint16), W, [0, 28])
+    np.testing.assert_allclose(logp, -math.log(V), rtol=0, atol=1e-15)
+    np.testing.assert_allclose(lse, math.log(V), rtol=0, atol=1e-15)
+    # out-of-range targets have no log-probability; lse is unaffected
+    h = randn_bits(rng, (3, D))
+    logp, lse = oracle.token_logprob(h, W, [-1, V, 3])
+    assert np.isnan(logp[0]) and np.isnan(logp[1]) and np.isfinite(logp[2])
+    assert np.all(np.isfinite(lse))
+
+
+def test_logprob_normalised_and_shift_invariant():
+    rng = np.random.default_rng(73)
+    V, D = 23, 16
+    # small integers: every product and sum below is exact in bf16 and fp64
+    h = bf16_bits(rng.integers(-2, 3, size=(1, D)))
+    W = bf16_bits(rng.integers(-2, 3, size=(V, D)))
+    all_t = np.arange(V, dtype=np.int32)
+    logp, _ = oracle.token_logprob(np.repeat(h, V, 0), W, all_t)
+    assert abs(math.fsum(np.exp(logp)) - 1.0) < 1e-14
+    # adding one vector w0 to every row shifts all logits by <h, w0>: no change
+    w0 = rng.integers(-2, 3, size=D)
+    W2 = bf16_bits(bits_f64(W) + w0)
+    logp2, lse2 = oracle.token_logprob(np.repeat(h, V, 0), W2, all_t)
+    np.testing.assert_allclose(logp2, logp, rtol=0, atol=1e-13)
+    shift = float(bits_f64(h)[0] @ w0)
+    _, lse1 = oracle.token_logprob(np.repeat(h, V, 0), W, all_t)
+    np.testing.assert_allclose(lse2, lse1 + shift, rtol=0, atol=1e-12)
