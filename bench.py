@@ -23,7 +23,9 @@ unmasked query-key pairs, two matrix products each) is reported beside it.
 85 % decode rows / 15 % append rows, log-normal contexts: page write, decode,
 append on one stream) beside its lower bounds at the published peaks.
 `shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
-rollouts whose rows share each task's prompt pages.
+rollouts whose rows share each task's prompt pages. `token_logprob` times the
+fused LM-head log-probability kernel at the Qwen3-8B head for 64 and 1024
+tokens.
 `cpu_baseline` is the fp64 CPU oracle on a bounded sample of the same inputs.
 """
 import argparse
@@ -289,6 +291,44 @@ def shared_prefix_leg(ra, synth, dev, steps: int, warmup: int):
     return res
 
 
+def logprob_leg(ra, synth, dev, steps: int, warmup: int):
+    """token_logprob on the Qwen3-8B LM head (V = 151936, D = 4096): a decode
+    batch of 64 tokens (bound by reading W) and 1024 tokens (bound by the
+    products)."""
+    import torch
+
+    V, D = 151936, 4096
+    gen = synth.value_generator(7, dev)
+    W = (synth.randn_bf16((V, D), gen, dev).float() * (1.0 / math.sqrt(D))).to(torch.bfloat16)
+    res = {"workload": f"token log-probabilities, LM head V={V} D={D} (Qwen3-8B), bf16"}
+    for N in (64, 1024):
+        h = synth.randn_bf16((N, D), gen, dev)
+        t = torch.randint(0, V, (N,), dtype=torch.int32, device=dev, generator=gen)
+        out = torch.empty(N, dtype=torch.float32, device=dev)
+        ws = torch.empty(ra.token_logprob_workspace_size(N, V), dtype=torch.uint8, device=dev)
+        for _ in range(warmup):
+            ra.token_logprob(h, W, t, 1.0, out=out, workspace=ws)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for e in ev:
+            e[0].record()
+            ra.token_logprob(h, W, t, 1.0, out=out, workspace=ws)
+            e[1].record()
+        torch.cuda.synchronize()
+        ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+        nbytes = V * D * 2 + N * D * 2 + N * 8
+        flops = 2 * N * V * D
+        gbs, tfs = nbytes / (ms * 1e-3) / 1e9, flops / (ms * 1e-3) / 1e12
+        res[f"N{N}"] = {"ms": round(ms, 4), "algorithmic_bytes": nbytes,
+                        "algorithmic_flops": flops, "GB_s": round(gbs, 1),
+                        "TFLOP_s": round(tfs, 1),
+                        "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+                        "frac_bf16_peak": round(tfs / BF16_PEAK_TFLOPS, 4)}
+        del h, t, out, ws
+    del W
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -299,6 +339,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-shared-prefix", action="store_true",
                     help="skip the shared-prefix decode leg (8 tasks x 8 rollouts)")
+    ap.add_argument("--no-logprob", action="store_true",
+                    help="skip the token log-probability leg (Qwen3-8B LM head)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-step leg (B = 512, 85 %% decode / 15 %% append rows)")
     ap.add_argument("--only", choices=["write", "decode", "append", "copy"],
@@ -403,6 +445,9 @@ def main():
     shared = None
     if not args.no_shared_prefix:
         shared = shared_prefix_leg(ra, synth, dev, args.steps, args.warmup)
+    logprob = None
+    if not args.no_logprob:
+        logprob = logprob_leg(ra, synth, dev, args.steps, args.warmup)
     mixed = None
     if not args.no_mixed:
         mixed = mixed_step(ra, synth, dev, min(args.steps, 10), min(args.warmup, 2))
@@ -455,6 +500,7 @@ def main():
                             "traffic": measured_traffic("append")},
         "mixed_step": mixed,
         "shared_prefix_decode": shared,
+        "token_logprob": logprob,
         "cpu_baseline": cpu_dec,
         "cpu_baseline_append": cpu_app,
     }

@@ -189,6 +189,32 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                         float *lse, hipStream_t stream);
 
 /*
+ * Token log-probabilities under an LM head: for each position n, the
+ * log-probability of the emitted token targets[n] (Sec. 3.3.3: token-in /
+ * token-out returns every generated token with its log-probability), fused
+ * into one pass over the LM-head matrix without writing the logits:
+ *   z_v = scale * <h[n], W[v]>,  lse[n] = ln sum_v exp z_v,
+ *   logprob[n] = z_{targets[n]} - lse[n]   (NaN if targets[n] is not in [0, V))
+ * bf16 inputs, fp32 products and outputs.
+ *
+ *   h          bf16 [N][D] hidden states (row n: the position's last-layer output)
+ *   W          bf16 [V][D] LM-head matrix, one row per vocabulary entry
+ *   targets    int32 [N]
+ *   scale      multiplies the logits (1 / temperature; 1 for the raw model)
+ *   logprob    fp32 [N]
+ *   lse        fp32 [N] or NULL
+ *   workspace  device scratch of at least token_logprob_workspace_size(N, V)
+ *              bytes (per-chunk partials; contents on entry ignored)
+ * Errors: RA_ERR_NULL; RA_ERR_SHAPE (N < 0, V <= 0, D <= 0);
+ *         RA_ERR_UNSUPPORTED (D not a multiple of 64); RA_ERR_WORKSPACE;
+ *         RA_ERR_HIP. N == 0 returns RA_OK without launching anything.
+ */
+size_t token_logprob_workspace_size(int32_t N, int32_t V);
+int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t N, int32_t V,
+                  int32_t D, float scale, float *logprob, float *lse, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Page write: scatter new tokens' keys and values into their pages, a bit
  * copy. Row b's new tokens are packed rows cu_new[b] .. cu_new[b+1]-1 of
  * k_new / v_new; token t of the row goes to logical position start_pos[b] + t.

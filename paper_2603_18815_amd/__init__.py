@@ -24,8 +24,9 @@ PAGE_SIZE = 16
 HEAD_DIM = 128
 
 __all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "kv_page_write",
-           "kv_page_gather", "decode_workspace_size", "decode_shared_prefix_workspace_size",
-           "abi_version", "RolloutAttnError"]
+           "kv_page_gather", "token_logprob", "decode_workspace_size",
+           "decode_shared_prefix_workspace_size", "token_logprob_workspace_size", "abi_version",
+           "RolloutAttnError"]
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -279,3 +280,43 @@ def kv_page_gather(kv: PagedKV, lens: torch.Tensor, cu_out: torch.Tensor,
         ctypes.byref(s), lens.data_ptr(), cu_out.data_ptr(), B, total, max_len,
         k_out.data_ptr(), v_out.data_ptr(), _stream(dev, stream)))
     return k_out, v_out
+
+
+def token_logprob_workspace_size(N: int, V: int) -> int:
+    return int(_lib.load().token_logprob_workspace_size(N, V))
+
+
+def token_logprob(h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, scale: float = 1.0,
+                  out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                  want_lse: bool = False, workspace: Optional[torch.Tensor] = None, stream=None
+                  ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Log-probability of targets[n] under logits scale * h[n] . W^T.
+
+    h bf16 [N][D], W bf16 [V][D], targets int32 [N] -> logprob fp32 [N] (, lse fp32 [N]).
+    """
+    lib = _lib.load()
+    dev = h.device
+    _need(h, "h", torch.bfloat16, dev)
+    _need(W, "W", torch.bfloat16, dev)
+    _need(targets, "targets", torch.int32, dev)
+    N, D = h.shape
+    V = W.shape[0]
+    _shape(W, (V, D), "W")
+    _shape(targets, (N,), "targets")
+    if out is None:
+        out = torch.empty((N,), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, dev)
+    _shape(out, (N,), "out")
+    if lse is None and want_lse:
+        lse = torch.empty((N,), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+        _shape(lse, (N,), "lse")
+    if workspace is None:
+        workspace = torch.empty(max(lib.token_logprob_workspace_size(N, V), 1),
+                                dtype=torch.uint8, device=dev)
+    _need(workspace, "workspace", torch.uint8, dev)
+    _lib.check("token_logprob", lib.token_logprob(
+        h.data_ptr(), W.data_ptr(), targets.data_ptr(), N, V, D, float(scale), out.data_ptr(),
+        _ptr(lse), workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
+    return out, lse

@@ -22,6 +22,8 @@ EXPORTS = (
     "rollout_attn_append",
     "kv_page_write",
     "kv_page_gather",
+    "token_logprob_workspace_size",
+    "token_logprob",
 )
 
 
@@ -75,6 +77,10 @@ def load() -> ctypes.CDLL:
     lib.rollout_attn_append.argtypes = [vp, vp, vp, kvp, i32, i32, i32, i32, i32, f32, vp, vp,
                                         vp]
     lib.rollout_attn_append.restype = ctypes.c_int
+    lib.token_logprob_workspace_size.argtypes = [i32, i32]
+    lib.token_logprob_workspace_size.restype = sz
+    lib.token_logprob.argtypes = [vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, sz, vp]
+    lib.token_logprob.restype = ctypes.c_int
     lib.kv_page_write.argtypes = [vp, vp, vp, vp, kvp, i32, i32, i32, i32, vp]
     lib.kv_page_write.restype = ctypes.c_int
     lib.kv_page_gather.argtypes = [kvp, vp, vp, i32, i32, i32, vp, vp, vp]

@@ -131,6 +131,25 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                                       scale, out, lse, stream));
 }
 
+size_t token_logprob_workspace_size(int32_t N, int32_t V) {
+  if (N <= 0 || V <= 0) return 0;
+  return ra::logprob_workspace_bytes(N, V);
+}
+
+int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t N, int32_t V,
+                  int32_t D, float scale, float *logprob, float *lse, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream) {
+  if (N < 0 || V <= 0 || D <= 0) return RA_ERR_SHAPE;
+  if (!h || !W || !targets || !logprob) return RA_ERR_NULL;
+  if (D % 64 != 0) return RA_ERR_UNSUPPORTED;
+  if (N == 0) return RA_OK;
+  if (ra::logprob_grid(N, V) > 0x7fffffff) return RA_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < ra::logprob_workspace_bytes(N, V)) return RA_ERR_WORKSPACE;
+  return hip_status(ra::launch_logprob(static_cast<const uint16_t *>(h),
+                                       static_cast<const uint16_t *>(W), targets, N, V, D, scale,
+                                       logprob, lse, workspace, stream));
+}
+
 int kv_page_write(const void *k_new, const void *v_new, const int32_t *cu_new,
                   const int32_t *start_pos, const ra_paged_kv *kv, int32_t B, int32_t total_new,
                   int32_t max_new, int32_t max_pos, hipStream_t stream) {

@@ -55,6 +55,14 @@ hipError_t launch_append(const uint16_t *q, const int32_t *cu_q, const int32_t *
                          int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
                          float *lse, hipStream_t stream);
 
+// ---- per-token log-probabilities under an LM head ----
+int32_t logprob_chunks(int32_t V);
+size_t logprob_workspace_bytes(int32_t N, int32_t V);
+int64_t logprob_grid(int32_t N, int32_t V);
+hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *targets, int32_t N,
+                          int32_t V, int32_t D, float scale, float *logp, float *lse,
+                          void *workspace, hipStream_t stream);
+
 // ---- page write / gather ----
 hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
                              const int32_t *start_pos, const PagedKV &kv, int32_t B,

@@ -1,0 +1,289 @@
+// Per-token log-probabilities under an LM head, fused: logits, log-sum-exp and
+// the gather of the emitted token's logit, without writing the logits.
+//
+// For token n (hidden state h[n], emitted token t[n]) and the LM-head matrix
+// W [V][D]: z_v = scale * <h[n], W[v]>, lse = ln sum_v exp z_v, and
+// logp = z_t - lse.
+//
+// Partial kernel: one workgroup (4 waves) per (128-row vocabulary chunk,
+// token block of 128, or 64 when N <= 64). Each wave computes the logits of
+// its 32 vocabulary rows for the block's tokens on the matrix cores (4 or 2
+// tiles of
+// mfma_f32_32x32x16_bf16: A = W rows, B = h^T). The loop walks D in steps of
+// 64 dims. W comes straight from memory, three steps ahead: a lane reads 64
+// contiguous bytes of its row per step, the two lanes of a row 128 bytes. The
+// block's h slice (tokens x 64 dims) is requested two steps ahead, staged once
+// per step into LDS (double-buffered, rows padded to 144 B: conflict-free) and
+// read by all four waves. The 64 dims of a step are split over the four products as lanes 0-31
+// dims 8u + 0..7 and lanes 32-63 dims 32 + 8u + 0..7 (any split of the
+// contraction is valid as long as A and B use the same one). The wave reduces
+// its logits to a (max, sum of exp) pair per token in base 2, the four waves
+// merge through LDS, and the workgroup writes one partial per (token, chunk);
+// the workgroup whose chunk holds token n's target stores that logit. The
+// grid is mapped so that the token blocks of one vocabulary chunk run on one
+// XCD and re-read the chunk from that XCD's L2.
+//
+// Combine kernel: one wave per token merges its partials in chunk order:
+// M = max_c m_c, L = sum_c l_c 2^(m_c - M), lse = (M + log2 L) ln 2.
+#include "ra_device.h"
+#include "ra_internal.h"
+
+namespace ra {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kLpWaves = 4;
+constexpr int kLpThreads = kLpWaves * kWave;
+constexpr int kVocabChunk = 32 * kLpWaves;    // vocabulary rows per workgroup
+constexpr int kMaxTiles = 4;                  // 32-token tiles per workgroup (largest variant)
+constexpr int kDimStep = 64;                  // dims per loop step (4 products)
+constexpr int kXcds = 8;                      // XCDs of an MI355X
+constexpr int kHPitch = kDimStep + 8;         // LDS row pitch of the h slice (elements)
+
+struct LogprobArgs {
+  const uint16_t *h;
+  const uint16_t *W;
+  const int32_t *targets;
+  float *ws_m;    // [N][chunks] running max, base-2 units
+  float *ws_l;    // [N][chunks] sum of 2^(y - max)
+  float *tgt;     // [N] logit of the target (natural units)
+  int32_t N, V, D, chunks, token_blocks;
+  float scale;        // logits = scale * <h, W_v>
+  float scale_log2;   // scale * log2(e)
+};
+
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Max / sum over lanes l and l ^ 32 (v_permlane32_swap gives each lane both).
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// kTiles 32-token tiles per workgroup: 2 for small batches (N <= 64), else 4.
+template <int kTiles>
+__global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobArgs a) {
+  constexpr int kTokenBlock = 32 * kTiles;
+  // XCD-aware placement: workgroup ids are dealt to the XCDs round-robin, so
+  // ids id, id + 8, id + 16, ... share an XCD; those consecutive "slots" get
+  // the token blocks of one vocabulary chunk.
+  const int id = blockIdx.x;
+  const int xcd = id % kXcds, slot = id / kXcds;
+  const int chunk = (slot / a.token_blocks) * kXcds + xcd;
+  const int tblock = slot - (slot / a.token_blocks) * a.token_blocks;
+  if (chunk >= a.chunks) return;
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int col = lane & 31, half = lane >> 5;
+  const int v0 = chunk * kVocabChunk + wave * 32;       // first vocabulary row of this wave
+  const int t0 = tblock * kTokenBlock;                  // first token of the block
+
+  // A row (vocabulary) this lane supplies, clamped into range for the loads;
+  // rows past V are masked after the products.
+  const uint16_t *wp = a.W + (size_t)min(v0 + col, a.V - 1) * a.D + 32 * half;
+  // h staging: thread i copies 16-byte chunks i + 256 j (j = 0..3) of the
+  // block's 128 x 64 slice (token = chunk / 8, 8 dims per chunk); tokens past
+  // N are clamped (their columns are never written back).
+  constexpr int kHChunks = kTokenBlock * kDimStep / 8 / kLpThreads;   // 2 or 4
+  __shared__ __attribute__((aligned(16))) uint16_t s_h[2][kTokenBlock * kHPitch];
+  const uint16_t *hsrc[kHChunks];
+  int hdst[kHChunks];
+#pragma unroll
+  for (int i = 0; i < kHChunks; ++i) {
+    const int c = threadIdx.x + kLpThreads * i, tok = c >> 3, d8 = (c & 7) * 8;
+    hsrc[i] = a.h + (size_t)min(t0 + tok, a.N - 1) * a.D + d8;
+    hdst[i] = tok * kHPitch + d8;
+  }
+  // Two register sets for h (requested two steps ahead) and four for W
+  // (three steps ahead); the loop body is four steps so that every set keeps
+  // a fixed role and no operand is copied.
+  u32x4 hx[kHChunks], hy[kHChunks];
+  auto h_load = [&](u32x4 *dst, int s) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kHChunks; ++i) dst[i] = load_u32x4(hsrc[i] + s * kDimStep);
+  };
+  auto h_store = [&](int buf, const u32x4 *src) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kHChunks; ++i) store_u32x4(&s_h[buf][hdst[i]], src[i]);
+  };
+  bf16x8 w0[4], w1[4], w2[4], w3[4];
+  auto w_load = [&](bf16x8 *dst, int s) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) dst[u] = load_bf16x8(wp + s * kDimStep + 8 * u);
+  };
+  const int nsteps = a.D / kDimStep;
+  const int last = nsteps - 1;
+  f32x16 acc[kTiles];
+#pragma unroll
+  for (int tt = 0; tt < kTiles; ++tt) acc[tt] = f32x16{};
+  // Step s: request h(s + 2) into `hf` and W(s + 3) into `wf` (past the last
+  // step the requests repeat it: branch-free, exact wait counts), run the
+  // products of step s on `wu` and LDS buffer s & 1, then store h(s + 1)
+  // (register set `hs`) into the other buffer.
+  auto step = [&](int s, const bf16x8 *wu, bf16x8 *wf, u32x4 *hf, const u32x4 *hs)
+      __attribute__((always_inline)) {
+    h_load(hf, min(s + 2, last));
+    w_load(wf, min(s + 3, last));
+    const uint16_t *hb = &s_h[s & 1][col * kHPitch + 32 * half];
+#pragma unroll
+    for (int tt = 0; tt < kTiles; ++tt) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bf16x8 b = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4 *>(hb + 32 * tt * kHPitch + 8 * u));
+        acc[tt] = mfma32x32x16(wu[u], b, acc[tt]);
+      }
+    }
+    h_store((s + 1) & 1, hs);
+    __syncthreads();
+  };
+
+  h_load(hx, 0);
+  h_load(hy, min(1, last));
+  w_load(w0, 0);
+  w_load(w1, min(1, last));
+  w_load(w2, min(2, last));
+  h_store(0, hx);
+  __syncthreads();
+  // step s uses W set s % 4 and h register set (s + 1) % 2 for the store
+  int s = 0;
+  for (; s + 4 <= nsteps; s += 4) {
+    step(s, w0, w3, hx, hy);
+    step(s + 1, w1, w0, hy, hx);
+    step(s + 2, w2, w1, hx, hy);
+    step(s + 3, w3, w2, hy, hx);
+  }
+  if (s < nsteps) step(s, w0, w3, hx, hy);
+  if (s + 1 < nsteps) step(s + 1, w1, w0, hy, hx);
+  if (s + 2 < nsteps) step(s + 2, w2, w1, hx, hy);
+
+  // Lane l holds, for token column t0 + 32 tt + col, the logits of vocabulary
+  // rows v0 + 8 (r / 4) + 4 half + r % 4, r = 0..15.
+  __shared__ float s_m[kLpWaves][kTokenBlock];
+  __shared__ float s_l[kLpWaves][kTokenBlock];
+#pragma unroll
+  for (int tt = 0; tt < kTiles; ++tt) {
+    const int t = t0 + 32 * tt + col;
+    const int target = t < a.N ? a.targets[t] : -1;
+    float y[16];
+    float m = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int v = v0 + 8 * (r >> 2) + 4 * half + (r & 3);
+      y[r] = v < a.V ? acc[tt][r] * a.scale_log2 : -INFINITY;
+      m = fmaxf(m, y[r]);
+      if (v == target) a.tgt[t] = acc[tt][r] * a.scale;
+    }
+    m = pair_max(m);
+    const float m_use = m == -INFINITY ? 0.f : m;
+    float sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sum += fast_exp2(y[r] - m_use);
+    sum = pair_sum(sum);
+    if (half == 0) {
+      s_m[wave][32 * tt + col] = m;
+      s_l[wave][32 * tt + col] = sum;
+    }
+  }
+  __syncthreads();
+
+  // Merge the four waves: one thread per token of the block.
+  const int c = threadIdx.x;
+  if (c < kTokenBlock && t0 + c < a.N) {
+    float M = s_m[0][c];
+#pragma unroll
+    for (int w = 1; w < kLpWaves; ++w) M = fmaxf(M, s_m[w][c]);
+    const float M_use = M == -INFINITY ? 0.f : M;
+    float L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kLpWaves; ++w) L += s_l[w][c] * fast_exp2(s_m[w][c] - M_use);
+    const size_t part = (size_t)(t0 + c) * a.chunks + chunk;
+    a.ws_m[part] = M;
+    a.ws_l[part] = L;
+  }
+}
+
+__global__ __launch_bounds__(kLpThreads) void logprob_combine_kernel(LogprobArgs a, float *logp,
+                                                                   float *lse) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t = blockIdx.x * kLpWaves + threadIdx.x / kWave;
+  if (t >= a.N) return;
+  const float *m = a.ws_m + (size_t)t * a.chunks;
+  const float *l = a.ws_l + (size_t)t * a.chunks;
+  // Each lane folds chunks lane, lane + 64, ... in order; the lanes are then
+  // combined by a fixed butterfly, so the result does not depend on timing.
+  float M = -INFINITY;
+  for (int c = lane; c < a.chunks; c += kWave) M = fmaxf(M, m[c]);
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
+  float L = 0.f;
+  for (int c = lane; c < a.chunks; c += kWave) L += l[c] * fast_exp2(m[c] - M);
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) L += __shfl_xor(L, o);
+  if (lane == 0) {
+    const float ls = (M + __log2f(L)) * kLn2;
+    const int target = a.targets[t];
+    logp[t] = target >= 0 && target < a.V ? a.tgt[t] - ls : __builtin_nanf("");
+    if (lse) lse[t] = ls;
+  }
+}
+
+}  // namespace
+
+int32_t logprob_chunks(int32_t V) { return (V + kVocabChunk - 1) / kVocabChunk; }
+
+size_t logprob_workspace_bytes(int32_t N, int32_t V) {
+  return ((size_t)N * logprob_chunks(V) * 2 + (size_t)N) * sizeof(float);
+}
+
+namespace {
+int logprob_tiles(int32_t N) { return N <= 64 ? 2 : kMaxTiles; }
+}  // namespace
+
+int64_t logprob_grid(int32_t N, int32_t V) {
+  const int64_t chunks_pad = (logprob_chunks(V) + kXcds - 1) / kXcds * kXcds;
+  const int block = 32 * logprob_tiles(N);
+  return chunks_pad * ((N + block - 1) / block);
+}
+
+hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *targets, int32_t N,
+                          int32_t V, int32_t D, float scale, float *logp, float *lse,
+                          void *workspace, hipStream_t stream) {
+  LogprobArgs a;
+  a.h = h;
+  a.W = W;
+  a.targets = targets;
+  a.N = N;
+  a.V = V;
+  a.D = D;
+  a.chunks = logprob_chunks(V);
+  const int tiles = logprob_tiles(N);
+  a.token_blocks = (N + 32 * tiles - 1) / (32 * tiles);
+  a.ws_m = static_cast<float *>(workspace);
+  a.ws_l = a.ws_m + (size_t)N * a.chunks;
+  a.tgt = a.ws_l + (size_t)N * a.chunks;
+  a.scale = scale;
+  a.scale_log2 = scale * kLog2e;
+  const dim3 grid((unsigned)logprob_grid(N, V));
+  if (tiles == 2)
+    hipLaunchKernelGGL(logprob_partial_kernel<2>, grid, dim3(kLpThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(logprob_partial_kernel<kMaxTiles>, grid, dim3(kLpThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(logprob_combine_kernel, dim3((N + kLpWaves - 1) / kLpWaves),
+                     dim3(kLpThreads), 0, stream, a, logp, lse);
+  return hipGetLastError();
+}
+
+}  // namespace ra

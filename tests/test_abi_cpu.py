@@ -109,6 +109,25 @@ def test_shared_prefix_decode_validation(lib):
     assert f(0, 32, 8, 32768, 8192) == 0
 
 
+def test_token_logprob_validation(lib):
+    def call(**kw):
+        d = dict(h=FAKE, W=FAKE, t=FAKE, N=8, V=100, D=128, out=FAKE, ws=FAKE, ws_bytes=1 << 30)
+        d.update(kw)
+        return lib.token_logprob(d["h"], d["W"], d["t"], d["N"], d["V"], d["D"], 1.0, d["out"],
+                                 None, d["ws"], d["ws_bytes"], None)
+    assert call(h=None) == _lib.RA_ERR_NULL
+    assert call(out=None) == _lib.RA_ERR_NULL
+    assert call(N=-1) == _lib.RA_ERR_SHAPE
+    assert call(V=0) == _lib.RA_ERR_SHAPE
+    assert call(D=0) == _lib.RA_ERR_SHAPE
+    assert call(D=96) == _lib.RA_ERR_UNSUPPORTED       # not a multiple of 64
+    assert call(ws_bytes=4) == _lib.RA_ERR_WORKSPACE
+    assert call(N=0) == _lib.RA_OK
+    f = lib.token_logprob_workspace_size
+    assert f(0, 100) == 0 and f(8, 0) == 0
+    assert f(64, 151936) == (64 * 1187 * 2 + 64) * 4     # 1187 chunks of 128 rows
+
+
 def test_append_validation(lib):
     def call(kv, **kw):
         d = dict(q=FAKE, cu=FAKE, ctx=FAKE, B=2, Hq=4, total_q=10, max_q=5, max_kv=64,

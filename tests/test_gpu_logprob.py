@@ -1,0 +1,106 @@
+"""GPU parity of token_logprob (through the C ABI) against the fp64 CPU oracle.
+
+Tolerance: the library accumulates each logit in fp32 over D products of
+exactly-widened bf16 values (the products are exact) and uses the hardware
+exp2/log2 (about 1 ulp); the oracle is fp64. Rounding in a sum of D terms
+behaves like a random walk, about sqrt(D) * 2^-24 * |terms| ~ 1e-6 for the
+inputs here (logits of order 1-10, D <= 4096), against a loose worst case of
+D * 2^-24 * sum_k |h_k W_vk|. Every log-probability and lse must agree within
+1e-4 absolute; out-of-range targets must give NaN.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_18815_amd as ra
+import synth
+from tests.gpu_util import bits
+
+pytestmark = pytest.mark.gpu
+ATOL = 1e-4
+
+
+def say(msg):
+    print(f"[gpu-test] {msg}", flush=True)
+
+
+def inputs(seed, N, V, D, dev, w_scale=None):
+    """h ~ N(0,1), W ~ N(0, 1/D) (logits of order 1), both rounded to bf16."""
+    gen = synth.value_generator(seed, dev)
+    h = synth.randn_bf16((N, D), gen, dev)
+    W = synth.randn_bf16((V, D), gen, dev)
+    s = 1.0 / math.sqrt(D) if w_scale is None else w_scale
+    W = (W.float() * s).to(torch.bfloat16)
+    return h, W
+
+
+def check(lp, ls, ref_lp, ref_ls, what):
+    lp, ls = lp.cpu().numpy().astype(np.float64), ls.cpu().numpy().astype(np.float64)
+    ok = ~np.isnan(ref_lp)
+    assert np.all(np.isnan(lp[~ok])), f"{what}: out-of-range targets must give NaN"
+    err_lp = float(np.abs(lp[ok] - ref_lp[ok]).max()) if ok.any() else 0.0
+    err_ls = float(np.abs(ls - ref_ls).max())
+    print(f"[parity] {what}: max|dlogp|={err_lp:.2e} max|dlse|={err_ls:.2e}", flush=True)
+    assert err_lp <= ATOL and err_ls <= ATOL, (what, err_lp, err_ls)
+
+
+@pytest.mark.parametrize("N,V,D,scale", [
+    (70, 1000, 128, 1.0),    # two token blocks (ragged), a ragged last vocabulary chunk
+    (5, 257, 192, 0.7),      # temperature scale, vocabulary of 2 chunks + 1 row
+    (1, 1, 64, 1.0),         # a single vocabulary entry: logp = 0
+    (130, 4096, 256, 1.0),   # three token blocks, 32 chunks (4 per XCD)
+])
+def test_token_logprob_vs_oracle(device, N, V, D, scale):
+    say(f"token_logprob N={N} V={V} D={D} scale={scale}")
+    h, W = inputs(N + V + D, N, V, D, device)
+    rng = np.random.default_rng(N + V)
+    t = rng.integers(0, V, size=N).astype(np.int32)
+    if N >= 5:
+        t[:4] = [0, V - 1, -1, V]           # first and last id, two out of range
+    lp, ls = ra.token_logprob(h, W, torch.as_tensor(t, device=device), scale, want_lse=True)
+    torch.cuda.synchronize()
+    ref_lp, ref_ls = oracle.token_logprob(bits(h), bits(W), t, scale)
+    check(lp, ls, ref_lp, ref_ls, f"N={N} V={V} D={D}")
+    if V == 1:
+        assert torch.all(lp == 0)
+
+
+def test_token_logprob_peaked_and_flat(device):
+    """Large logits (a peaked distribution) and zero hidden states (uniform)."""
+    N, V, D = 40, 3000, 128
+    h, W = inputs(5, N, V, D, device, w_scale=0.5)     # logits of order 5-20
+    h[:8] = 0                                           # uniform rows
+    t = torch.arange(N, dtype=torch.int32, device=device) * 71 % V
+    lp, ls = ra.token_logprob(h, W, t, 1.0, want_lse=True)
+    torch.cuda.synchronize()
+    ref_lp, ref_ls = oracle.token_logprob(bits(h), bits(W), t.cpu().numpy(), 1.0)
+    check(lp, ls, ref_lp, ref_ls, "peaked / flat")
+    np.testing.assert_allclose(lp[:8].cpu().numpy(), -math.log(V), atol=1e-5, rtol=0)
+
+
+def test_token_logprob_deterministic(device):
+    N, V, D = 64, 5000, 256
+    h, W = inputs(9, N, V, D, device)
+    t = torch.randint(0, V, (N,), dtype=torch.int32, device=device,
+                      generator=synth.value_generator(9, device))
+    a, la = ra.token_logprob(h, W, t, 1.0, want_lse=True)
+    b, lb = ra.token_logprob(h, W, t, 1.0, want_lse=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(la, lb)
+
+
+def test_token_logprob_qwen3_lm_head(device):
+    """The Qwen3-8B LM-head shape (V = 151936, D = 4096) for a decode batch of 64
+    tokens, every token against the oracle."""
+    N, V, D = 64, 151936, 4096
+    say(f"token_logprob Qwen3-8B LM head N={N}")
+    h, W = inputs(8, N, V, D, device)
+    t = torch.randint(0, V, (N,), dtype=torch.int32, device=device,
+                      generator=synth.value_generator(8, device))
+    lp, ls = ra.token_logprob(h, W, t, 1.0, want_lse=True)
+    torch.cuda.synchronize()
+    ref_lp, ref_ls = oracle.token_logprob(bits(h), bits(W), t.cpu().numpy(), 1.0)
+    check(lp, ls, ref_lp, ref_ls, "Qwen3-8B LM head, 64 tokens")
