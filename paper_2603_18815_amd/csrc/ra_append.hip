@@ -28,6 +28,7 @@ namespace ra {
 namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * kWave;
@@ -130,8 +131,10 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
   const int wave_q0 = ctx + i0 + (wave * kRowsPerWave) / G;
 
   // ---- staging: pass p moves pages 2p, 2p + 1 of the block; each thread one
-  // 16-byte chunk of K and one of V.
-  const int st_page = tid >> 8, st_chunk = tid & 255;
+  // 16-byte chunk of K and one of V. The page index is wave-uniform (waves
+  // 0-3 stage the first page of a pass, 4-7 the second), so the block-table
+  // read and the page base run on the scalar unit.
+  const int st_page = __builtin_amdgcn_readfirstlane(tid >> 8), st_chunk = tid & 255;
   const int st_slot = st_chunk >> 4, st_kch = st_chunk & 15;   // K: slot, 16-B chunk
   const int st_d = st_chunk >> 1, st_half = st_chunk & 1;      // V: dim row, 8-slot half
   u32x4 kreg[kPasses], vreg[kPasses];
@@ -233,15 +236,29 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
       // stays below kSumLimit, which fp32 and bf16 carry without loss, and
       // out = O / l does not depend on when the max moves.
       f32x8 p0, p1;
+      bf16x8 pb0, pb1;
       float psum;
+      // Weights, rounded to bf16 for the P·V product, and their sum taken
+      // from the rounded values (two chains of bf16 pair dot products with
+      // (1, 1)), so that l normalises exactly the weights O accumulates.
       auto weights = [&]() __attribute__((always_inline)) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           p0[e] = fast_exp2(__builtin_fmaf(sc[e], cs, -m_run));
           p1[e] = fast_exp2(__builtin_fmaf(sc[8 + e], cs, -m_run));
         }
-        psum = (((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]))) +
-               (((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7])));
+        pb0 = to_bf16x8(p0);
+        pb1 = to_bf16x8(p1);
+        const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+        float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s0 = __builtin_amdgcn_fdot2_f32_bf16(
+              bf16x2{pb0[2 * e], pb0[2 * e + 1]}, one, s0, false);
+          s1 = __builtin_amdgcn_fdot2_f32_bf16(
+              bf16x2{pb1[2 * e], pb1[2 * e + 1]}, one, s1, false);
+        }
+        psum = s0 + s1;
       };
       weights();
       if (!__all(psum <= kSumLimit)) {
@@ -261,7 +278,6 @@ __global__ __launch_bounds__(kThreads, 1) void append_kernel(AppendArgs a) {
         weights();
       }
       l_run += psum;
-      const bf16x8 pb0 = to_bf16x8(p0), pb1 = to_bf16x8(p1);
       // O^T[d][qrow] += V^T[d][key] P^T[key][qrow]: page c of the pair, slots
       // 8 grp + 0..7, d = 32 dt + col.
 #pragma unroll
