@@ -21,7 +21,9 @@ unmasked query-key pairs, two matrix products each) is reported beside it.
 `roofline_append` the append kernel against the 2.5 PFLOP/s dense bf16 peak.
 `mixed_step` times the mixed rollout step on one pool (B = 512 trajectories,
 85 % decode rows / 15 % append rows, log-normal contexts: page write, decode,
-append on one stream) beside its lower bounds at the published peaks.
+append on one stream) beside its lower bounds at the published peaks, and the
+same step with decode and append rows in one persistent launch
+(`single_launch`).
 `shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
 rollouts whose rows share each task's prompt pages. `token_logprob` times the
 fused LM-head log-probability kernel at the Qwen3-8B head for 64 and 1024
@@ -184,6 +186,21 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
         if ev is not None:
             ev[3].record()
 
+    ws_mix = torch.empty(ra.mixed_workspace_size(w.kv_lens.shape[0], w.q_lens.shape[0], w.Hq,
+                                                 w.Hkv, w.Hkv, max_kv_d, max_q),
+                         dtype=torch.uint8, device=dev)
+
+    def step_single(ev=None):
+        if ev is not None:
+            ev[0].record()
+        ra.kv_page_write(t.k_new, t.v_new, cu_t, start_t, kv_w, max_new, max_pos)
+        if ev is not None:
+            ev[1].record()
+        ra.mixed(t.q_decode, kv_d, kv_lens, t.q_append, cu_q, ctx, kv_a, max_kv_d, max_q,
+                 max_kv_a, SCALE, out_decode=out_d, out_append=out_a, workspace=ws_mix)
+        if ev is not None:
+            ev[2].record()
+
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -191,6 +208,15 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
     for k in range(steps):
         step(events[k])
     torch.cuda.synchronize()
+    for _ in range(warmup):
+        step_single()
+    torch.cuda.synchronize()
+    ev_single = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for k in range(steps):
+        step_single(ev_single[k])
+    torch.cuda.synchronize()
+    single_ms = np.mean([e[0].elapsed_time(e[2]) for e in ev_single])
+    single_attn_ms = np.mean([e[1].elapsed_time(e[2]) for e in ev_single])
     w_ms = np.mean([e[0].elapsed_time(e[1]) for e in events])
     d_ms = np.mean([e[1].elapsed_time(e[2]) for e in events])
     a_ms = np.mean([e[2].elapsed_time(e[3]) for e in events])
@@ -212,8 +238,16 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
         "append_TFLOP_s": round(aflops / (a_ms * 1e-3) / 1e12, 1),
         "bound_sequential_ms": round(seq_ms, 3), "bound_overlap_ms": round(ovl_ms, 3),
         "frac_of_sequential_bound": round(seq_ms / s_ms, 4),
+        # decode and append rows in one persistent launch (rollout_attn_mixed)
+        "single_launch": {
+            "ms": round(float(single_ms), 4),
+            "attention_ms": round(float(single_attn_ms), 4),
+            "speedup_vs_separate": round(float(s_ms / single_ms), 4),
+            "frac_of_sequential_bound": round(seq_ms / single_ms, 4),
+            "frac_of_overlap_bound": round(ovl_ms / single_ms, 4),
+        },
     }
-    del t, out_d, out_a, ws
+    del t, out_d, out_a, ws, ws_mix
     torch.cuda.empty_cache()
     return res
 

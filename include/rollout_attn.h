@@ -189,6 +189,52 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                         float *lse, hipStream_t stream);
 
 /*
+ * Mixed step: the attention of one rollout step in which some trajectories
+ * decode a token while others have just had tool observations appended
+ * (Sec. 3.3.1: many rollout workers drive their agent loops concurrently, each
+ * firing LLM calls; Sec. 3.3.3: observations are appended to the retained
+ * tokens). Computes, in one persistent launch over the GPU (plus a one-
+ * workgroup planning kernel before it and the decode combine after it):
+ *   - for the decode rows, exactly what rollout_attn_decode computes
+ *     (up to rounding: each split is summed by twice as many waves);
+ *   - for the append rows, bitwise what rollout_attn_append computes.
+ * Append tiles are taken longest first and the decode splits are spread
+ * among them, so that decode's HBM traffic overlaps append's matrix work.
+ * The two sides may use different block tables (and pools); either side may
+ * be empty (B_decode == 0, or B_append == 0 / total_q == 0 / max_q_len == 0),
+ * in which case its pointers are not used and may be NULL.
+ *
+ *   decode side:  q_decode, kv_decode, kv_lens, B_decode, max_kv_len_decode,
+ *                 out_decode, lse_decode: as q, kv, kv_lens, B, max_kv_len,
+ *                 out, lse of rollout_attn_decode
+ *   append side:  q_append, cu_q, ctx_lens, kv_append, B_append, total_q,
+ *                 max_q_len, max_kv_len_append, out_append, lse_append: as q,
+ *                 cu_q, ctx_lens, kv, B, total_q, max_q_len, max_kv_len, out,
+ *                 lse of rollout_attn_append (the chunks' K/V already written)
+ *   Hq, scale     shared by both sides
+ *   workspace     device scratch of at least rollout_attn_mixed_workspace_size(
+ *                 B_decode, B_append, Hq, Hkv_decode, Hkv_append,
+ *                 max_kv_len_decode, max_q_len) bytes: work lists, a work
+ *                 counter and decode partials, all rewritten by every call
+ *                 (contents on entry are ignored). Calls that share a
+ *                 workspace must not overlap.
+ * Errors: as rollout_attn_decode / rollout_attn_append for each non-empty
+ *         side; RA_ERR_UNSUPPORTED also for more than 256 KV heads or more
+ *         than 2^31 - 2^16 work entries.
+ */
+size_t rollout_attn_mixed_workspace_size(int32_t B_decode, int32_t B_append, int32_t Hq,
+                                         int32_t Hkv_decode, int32_t Hkv_append,
+                                         int32_t max_kv_len_decode, int32_t max_q_len);
+int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
+                       const int32_t *kv_lens, int32_t B_decode, int32_t max_kv_len_decode,
+                       float *out_decode, float *lse_decode, const void *q_append,
+                       const int32_t *cu_q, const int32_t *ctx_lens, const ra_paged_kv *kv_append,
+                       int32_t B_append, int32_t total_q, int32_t max_q_len,
+                       int32_t max_kv_len_append, float *out_append, float *lse_append,
+                       int32_t Hq, float scale, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+
+/*
  * Token log-probabilities under an LM head: for each position n, the
  * log-probability of the emitted token targets[n] (Sec. 3.3.3: token-in /
  * token-out returns every generated token with its log-probability), fused

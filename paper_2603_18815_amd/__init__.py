@@ -23,10 +23,10 @@ from ._lib import RolloutAttnError  # noqa: F401  (re-export)
 PAGE_SIZE = 16
 HEAD_DIM = 128
 
-__all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "kv_page_write",
+__all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "mixed", "kv_page_write",
            "kv_page_gather", "token_logprob", "decode_workspace_size",
-           "decode_shared_prefix_workspace_size", "token_logprob_workspace_size", "abi_version",
-           "RolloutAttnError"]
+           "decode_shared_prefix_workspace_size", "mixed_workspace_size",
+           "token_logprob_workspace_size", "abi_version", "RolloutAttnError"]
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -229,6 +229,81 @@ def append(q: torch.Tensor, cu_q: torch.Tensor, ctx_lens: torch.Tensor, kv: Page
         q.data_ptr(), cu_q.data_ptr(), ctx_lens.data_ptr(), ctypes.byref(s), B, Hq, total_q,
         max_q_len, max_kv_len, float(scale), out.data_ptr(), _ptr(lse), _stream(dev, stream)))
     return out, lse
+
+
+def mixed_workspace_size(B_decode: int, B_append: int, Hq: int, Hkv_decode: int,
+                         Hkv_append: int, max_kv_len_decode: int, max_q_len: int) -> int:
+    return int(_lib.load().rollout_attn_mixed_workspace_size(
+        B_decode, B_append, Hq, Hkv_decode, Hkv_append, max_kv_len_decode, max_q_len))
+
+
+def mixed(q_decode: torch.Tensor, kv_decode: PagedKV, kv_lens: torch.Tensor,
+          q_append: torch.Tensor, cu_q: torch.Tensor, ctx_lens: torch.Tensor,
+          kv_append: PagedKV, max_kv_len_decode: Optional[int] = None,
+          max_q_len: Optional[int] = None, max_kv_len_append: Optional[int] = None,
+          scale: Optional[float] = None, out_decode: Optional[torch.Tensor] = None,
+          out_append: Optional[torch.Tensor] = None, want_lse: bool = False,
+          workspace: Optional[torch.Tensor] = None, stream=None):
+    """Decode rows and append rows of one step in one launch.
+
+    q_decode bf16 [Bd][Hq][128] -> out_decode fp32 [Bd][Hq][128];
+    q_append bf16 [total_q][Hq][128] -> out_append fp32 [total_q][Hq][128].
+    Returns (out_decode, out_append, lse_decode, lse_append); the lse entries
+    are None unless want_lse.
+    """
+    lib = _lib.load()
+    dev = q_decode.device
+    _need(q_decode, "q_decode", torch.bfloat16, dev)
+    _need(kv_lens, "kv_lens", torch.int32, dev)
+    _need(q_append, "q_append", torch.bfloat16, dev)
+    _need(cu_q, "cu_q", torch.int32, dev)
+    _need(ctx_lens, "ctx_lens", torch.int32, dev)
+    for kv in (kv_decode, kv_append):
+        if kv.device != dev:
+            raise ValueError(f"caches must be on {dev}, got {kv.device}")
+    Bd, Hq, D = q_decode.shape
+    total_q = q_append.shape[0]
+    _shape(q_decode, (Bd, Hq, HEAD_DIM), "q_decode")
+    _shape(q_append, (total_q, Hq, HEAD_DIM), "q_append")
+    _shape(kv_lens, (Bd,), "kv_lens")
+    Ba = ctx_lens.shape[0]
+    _shape(cu_q, (Ba + 1,), "cu_q")
+    _rows(kv_decode, Bd)
+    _rows(kv_append, Ba)
+    if max_kv_len_decode is None:
+        max_kv_len_decode = int(kv_lens.max().item()) if Bd else 0
+    if max_q_len is None or max_kv_len_append is None:
+        t = (cu_q[1:] - cu_q[:-1]) if Ba else cu_q[:0]
+        if max_q_len is None:
+            max_q_len = int(t.max().item()) if Ba else 0
+        if max_kv_len_append is None:
+            max_kv_len_append = int((t + ctx_lens).max().item()) if Ba else 0
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out_decode is None:
+        out_decode = torch.empty((Bd, Hq, D), dtype=torch.float32, device=dev)
+    if out_append is None:
+        out_append = torch.empty((total_q, Hq, D), dtype=torch.float32, device=dev)
+    _need(out_decode, "out_decode", torch.float32, dev)
+    _shape(out_decode, (Bd, Hq, HEAD_DIM), "out_decode")
+    _need(out_append, "out_append", torch.float32, dev)
+    _shape(out_append, (total_q, Hq, HEAD_DIM), "out_append")
+    lse_d = torch.empty((Bd, Hq), dtype=torch.float32, device=dev) if want_lse else None
+    lse_a = torch.empty((total_q, Hq), dtype=torch.float32, device=dev) if want_lse else None
+    ws_bytes = lib.rollout_attn_mixed_workspace_size(
+        Bd, Ba, Hq, kv_decode.num_kv_heads, kv_append.num_kv_heads, max_kv_len_decode,
+        max_q_len)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    _need(workspace, "workspace", torch.uint8, dev)
+    sd, sa = kv_decode.struct(), kv_append.struct()
+    _lib.check("rollout_attn_mixed", lib.rollout_attn_mixed(
+        q_decode.data_ptr(), ctypes.byref(sd), kv_lens.data_ptr(), Bd, max_kv_len_decode,
+        out_decode.data_ptr(), _ptr(lse_d), q_append.data_ptr(), cu_q.data_ptr(),
+        ctx_lens.data_ptr(), ctypes.byref(sa), Ba, total_q, max_q_len, max_kv_len_append,
+        out_append.data_ptr(), _ptr(lse_a), Hq, float(scale), workspace.data_ptr(),
+        workspace.numel(), _stream(dev, stream)))
+    return out_decode, out_append, lse_d, lse_a
 
 
 def kv_page_write(k_new: torch.Tensor, v_new: torch.Tensor, cu_new: torch.Tensor,

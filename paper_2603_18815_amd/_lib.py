@@ -20,6 +20,8 @@ EXPORTS = (
     "rollout_attn_decode_shared_prefix_workspace_size",
     "rollout_attn_decode_shared_prefix",
     "rollout_attn_append",
+    "rollout_attn_mixed_workspace_size",
+    "rollout_attn_mixed",
     "kv_page_write",
     "kv_page_gather",
     "token_logprob_workspace_size",
@@ -77,6 +79,12 @@ def load() -> ctypes.CDLL:
     lib.rollout_attn_append.argtypes = [vp, vp, vp, kvp, i32, i32, i32, i32, i32, f32, vp, vp,
                                         vp]
     lib.rollout_attn_append.restype = ctypes.c_int
+    lib.rollout_attn_mixed_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
+    lib.rollout_attn_mixed_workspace_size.restype = sz
+    lib.rollout_attn_mixed.argtypes = [vp, kvp, vp, i32, i32, vp, vp,
+                                       vp, vp, vp, kvp, i32, i32, i32, i32, vp, vp,
+                                       i32, f32, vp, sz, vp]
+    lib.rollout_attn_mixed.restype = ctypes.c_int
     lib.token_logprob_workspace_size.argtypes = [i32, i32]
     lib.token_logprob_workspace_size.restype = sz
     lib.token_logprob.argtypes = [vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, sz, vp]

@@ -15,7 +15,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "librollout_attn.so")
-SOURCES = ["ra_api.hip", "ra_page.hip", "ra_decode.hip", "ra_append.hip", "ra_logprob.hip"]
+SOURCES = ["ra_api.hip", "ra_page.hip", "ra_decode.hip", "ra_append.hip", "ra_mixed.hip",
+           "ra_logprob.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")

@@ -131,6 +131,72 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                                       scale, out, lse, stream));
 }
 
+size_t rollout_attn_mixed_workspace_size(int32_t B_decode, int32_t B_append, int32_t Hq,
+                                         int32_t Hkv_decode, int32_t Hkv_append,
+                                         int32_t max_kv_len_decode, int32_t max_q_len) {
+  if (B_decode < 0 || B_append < 0 || Hq <= 0 || max_kv_len_decode < 0 || max_q_len < 0)
+    return 0;
+  if (B_decode > 0 && (Hkv_decode <= 0 || Hq % Hkv_decode != 0)) return 0;
+  if (B_append > 0 && (Hkv_append <= 0 || Hq % Hkv_append != 0)) return 0;
+  if (B_decode == 0) Hkv_decode = B_append > 0 ? Hkv_append : 1;
+  if (B_append == 0) Hkv_append = Hkv_decode;
+  if (Hq / Hkv_append > 256) return 0;
+  return ra::mixed_layout(B_decode, B_append, Hq, Hkv_decode, Hkv_append, max_kv_len_decode,
+                          B_append > 0 ? max_q_len : 0)
+      .bytes;
+}
+
+int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
+                       const int32_t *kv_lens, int32_t B_decode, int32_t max_kv_len_decode,
+                       float *out_decode, float *lse_decode, const void *q_append,
+                       const int32_t *cu_q, const int32_t *ctx_lens, const ra_paged_kv *kv_append,
+                       int32_t B_append, int32_t total_q, int32_t max_q_len,
+                       int32_t max_kv_len_append, float *out_append, float *lse_append,
+                       int32_t Hq, float scale, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream) {
+  if (B_decode < 0 || B_append < 0 || Hq <= 0 || max_kv_len_decode < 0 || total_q < 0 ||
+      max_q_len < 0 || max_kv_len_append < 0)
+    return RA_ERR_SHAPE;
+  const bool dec = B_decode > 0;
+  const bool app = B_append > 0 && total_q > 0 && max_q_len > 0;
+  int s;
+  if (dec) {
+    if ((s = check_kv(kv_decode)) != RA_OK) return s;
+    if (!q_decode || !kv_lens || !out_decode) return RA_ERR_NULL;
+    if (Hq % kv_decode->num_kv_heads != 0) return RA_ERR_SHAPE;
+    if (Hq / kv_decode->num_kv_heads > 16 || B_decode > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+    if (!positions_fit(kv_decode, max_kv_len_decode)) return RA_ERR_SHAPE;
+  }
+  if (app) {
+    if ((s = check_kv(kv_append)) != RA_OK) return s;
+    if (!q_append || !cu_q || !ctx_lens || !out_append) return RA_ERR_NULL;
+    if (Hq % kv_append->num_kv_heads != 0) return RA_ERR_SHAPE;
+    if (Hq / kv_append->num_kv_heads > 256) return RA_ERR_UNSUPPORTED;
+    if (!positions_fit(kv_append, max_kv_len_append) || max_q_len > max_kv_len_append)
+      return RA_ERR_SHAPE;
+  }
+  if (!dec && !app) return RA_OK;
+  // an empty side borrows the other side's cache descriptor (never read)
+  const ra::PagedKV kd = to_internal(dec ? kv_decode : kv_append);
+  const ra::PagedKV ka = to_internal(app ? kv_append : kv_decode);
+  if (kd.hkv > ra::mixed_hkv_limit() || ka.hkv > ra::mixed_hkv_limit())
+    return RA_ERR_UNSUPPORTED;
+  const int32_t Bd = dec ? B_decode : 0, Ba = app ? B_append : 0;
+  const ra::MixedLayout layout = ra::mixed_layout(Bd, Ba, Hq, kd.hkv, ka.hkv, max_kv_len_decode,
+                                                  app ? max_q_len : 0);
+  // entries are named by int32 indices (and the counter runs one past the
+  // end per workgroup); query blocks and splits by 23 bits
+  if (layout.max_tiles + layout.max_splits > 0x7fffffff - 0xffff ||
+      layout.qblocks >= (1 << 23) || layout.plan.max_splits >= (1 << 23))
+    return RA_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < layout.bytes) return RA_ERR_WORKSPACE;
+  return hip_status(ra::launch_mixed(
+      static_cast<const uint16_t *>(q_decode), kd, kv_lens, Bd, max_kv_len_decode, out_decode,
+      lse_decode, static_cast<const uint16_t *>(q_append), cu_q, ctx_lens, ka, Ba, total_q,
+      max_q_len, max_kv_len_append, out_append, lse_append, Hq, scale, workspace, layout,
+      stream));
+}
+
 size_t token_logprob_workspace_size(int32_t N, int32_t V) {
   if (N <= 0 || V <= 0) return 0;
   return ra::logprob_workspace_bytes(N, V);

@@ -1,0 +1,373 @@
+// Append attention tile (causal chunked prefill against the paged cache),
+// shared by the append kernel and the mixed decode + append kernel.
+//
+// One workgroup (8 waves, two per SIMD) owns a block of QB = 256 / G
+// consecutive queries of one row and all G query heads of one KV head: 256
+// "query rows" (query, head), 32 per wave, each wave's rows forming the 32
+// columns of its 32x32 matrix tiles with their Q^T operands in registers.
+// The key loop walks the row's pages 64 keys (4 pages) at a time. Each block
+// of K and V is loaded once per workgroup into registers, stored to one of
+// two LDS buffers (the load of the next block is in flight while the current
+// one is used), one barrier per block, and all eight waves consume it:
+//   S^T[key][qrow] = K[key][:] · Q^T[:][qrow]        (bf16 mfma 32x32x16, fp32)
+//   O^T[d][qrow]  += V^T[d][key] · P^T[key][qrow]    (P rounded to bf16)
+// Keys are ordered inside each pair of pages so that the 16 S values a lane
+// receives are, in order, 8 consecutive slots of the first page and the same
+// 8 slots of the second: exactly the P^T operands of the two P·V products it
+// takes part in (no shuffles). Each query row stays in one lane column (two
+// lanes), so the online-softmax state is lane-local. Weights are taken
+// against a running max that moves only when they would grow too large
+// (a per-wave check on the weight sums), so the common path has no max
+// reduction and no cross-lane exchange. The causal mask (key position >
+// ctx + i) is applied only on blocks that reach past the wave's first query
+// position.
+#pragma once
+
+#include "ra_device.h"
+#include "ra_internal.h"
+
+// Everything lives in ra::atile, apart from the decode-split names (ra::dsplit)
+// that share a translation unit with it in the mixed kernel.
+namespace ra {
+namespace atile {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * kWave;
+constexpr int kRowsPerWave = 32;
+constexpr int kRowsPerGroup = kWaves * kRowsPerWave;   // 256
+constexpr int kBlock = 64;                             // keys per staged block
+constexpr int kBlockPages = kBlock / kPage;            // 4
+constexpr int kPagesPerPass = kThreads / 256;          // pages one staging pass covers
+constexpr int kPasses = kBlockPages / kPagesPerPass;   // 2
+constexpr int kBlockElems = kBlock * kHeadDim;         // per pool, per buffer
+constexpr float kSumLimit = 16384.f;                  // weight-sum bound between rescales
+
+struct AppendArgs {
+  const uint16_t *q;
+  const uint16_t *k_pool;
+  const uint16_t *v_pool;
+  const int32_t *block_table;
+  const int32_t *cu_q;
+  const int32_t *ctx_lens;
+  float *out;
+  float *lse;
+  int32_t hq, hkv, group, bt_stride, num_pages, total_q, max_q_len, max_kv_len, q_per_block;
+  float scale_log2;
+};
+
+// D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16). Lane l supplies A row
+// (l % 32) and B column (l % 32), contraction slots 8 (l / 32) + 0..7; it
+// receives D rows 8 (r / 4) + 4 (l / 32) + r % 4 of column l % 32, r = 0..15.
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Max of x over lanes l and l ^ 32 (one v_permlane32_swap: each lane gets
+// both values of its pair, in some order).
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ bf16x8 lds_bf16x8(const uint16_t *p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+}
+
+// LDS layouts (per buffer). K: 64 key rows x 128 dims, rows padded to
+// 272 B, so that 16 lanes reading the same chunk of 16 different rows (or 16
+// chunks of one row) fall on distinct banks, and a lane's eight operand reads
+// are one base address plus immediate offsets. V: [page][d][16 slots] (32 B
+// rows); the two 8-slot halves of row d are swapped when bit 3 of d is set,
+// for the same reason.
+constexpr int kKPitch = kHeadDim + 8;                   // K row pitch (elements)
+constexpr int kKBlockElems = kBlock * kKPitch;          // K buffer (elements)
+__device__ __forceinline__ int k_lds(int row, int chunk) { return row * kKPitch + chunk * 8; }
+__device__ __forceinline__ int v_lds(int page, int d, int half) {
+  return (page * kHeadDim + d) * kPage + ((half ^ ((d >> 3) & 1)) * 8);
+}
+
+// LDS of one tile: double-buffered K and V blocks.
+struct AppendLds {
+  __attribute__((aligned(16))) uint16_t k[2 * kKBlockElems];
+  __attribute__((aligned(16))) uint16_t v[2 * kBlockElems];
+};
+
+// Row b's chunk: its first query in q / out (cu0), its length T and the
+// tokens cached before it (ctx), clamped so that no access leaves the
+// caller's arrays. ctx < 0 marks a row whose chunk does not fit max_kv_len.
+struct AppendRow {
+  int cu0, T, ctx;
+};
+__device__ __forceinline__ AppendRow append_row(const AppendArgs &a, int b) {
+  AppendRow r;
+  r.cu0 = min(max(a.cu_q[b], 0), a.total_q);
+  r.T = min(min(max(a.cu_q[b + 1] - r.cu0, 0), a.max_q_len), a.total_q - r.cu0);
+  r.ctx = min(max(a.ctx_lens[b], 0), a.max_kv_len - r.T);
+  return r;
+}
+
+// Key blocks that query block qblk of row b walks (0: nothing to compute).
+__device__ __forceinline__ int append_tile_blocks(const AppendArgs &a, const AppendRow &r,
+                                                  int qblk) {
+  const int i0 = qblk * a.q_per_block;
+  if (i0 >= r.T || r.ctx < 0) return 0;
+  return (r.ctx + min(r.T, i0 + a.q_per_block) + kBlock - 1) / kBlock;
+}
+
+// One tile: query block qblk of row b, KV head g, by a workgroup of kThreads
+// threads. Every thread of the workgroup calls it with the same arguments.
+template <bool kPosScale>
+__device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g, int b,
+                                            AppendLds &lds) {
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  const int col = lane & 31, grp = lane >> 5;
+  const int G = a.group, QB = a.q_per_block;
+
+  const AppendRow row_ext = append_row(a, b);
+  const int cu0 = row_ext.cu0, T = row_ext.T, ctx = row_ext.ctx;
+  const int i0 = qblk * QB;
+  if (i0 >= T || ctx < 0) return;
+  const int i_end = min(T, i0 + QB);
+  const int row_end = ctx + T;                 // keys present in the cache for this row
+  const int kv_end = ctx + i_end;              // keys this workgroup attends to
+  const int row_pages = (row_end + kPage - 1) / kPage;
+  const int nblocks = (kv_end + kBlock - 1) / kBlock;
+  const int32_t *bt = a.block_table + (size_t)b * a.bt_stride;
+  const size_t head_stride = (size_t)kPage * kHeadDim;
+
+  uint16_t *const sK = lds.k;
+  uint16_t *const sV = lds.v;
+
+  // ---- this lane's query row and Q^T operands (dims 16 kk + 8 grp + 0..7) ----
+  const int r_wg = wave * kRowsPerWave + col;
+  const int qi = r_wg / G, hh = r_wg - qi * G;
+  const bool q_valid = r_wg < QB * G && i0 + qi < i_end;
+  const int qpos = q_valid ? ctx + i0 + qi : -1;
+  bf16x8 qop[8];
+  if (q_valid) {
+    const uint16_t *qp =
+        a.q + ((size_t)(cu0 + i0 + qi) * a.hq + (size_t)g * G + hh) * kHeadDim + 8 * grp;
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) qop[kk] = load_bf16x8(qp + 16 * kk);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) qop[kk] = bf16x8{};
+  }
+  // First query position of this wave (its rows are query-major).
+  const int wave_q0 = ctx + i0 + (wave * kRowsPerWave) / G;
+
+  // ---- staging: pass p moves pages 2p, 2p + 1 of the block; each thread one
+  // 16-byte chunk of K and one of V. The page index is wave-uniform (waves
+  // 0-3 stage the first page of a pass, 4-7 the second), so the block-table
+  // read and the page base run on the scalar unit.
+  const int st_page = __builtin_amdgcn_readfirstlane(tid >> 8), st_chunk = tid & 255;
+  const int st_slot = st_chunk >> 4, st_kch = st_chunk & 15;   // K: slot, 16-B chunk
+  const int st_d = st_chunk >> 1, st_half = st_chunk & 1;      // V: dim row, 8-slot half
+  u32x4 kreg[kPasses], vreg[kPasses];
+  auto stage_load = [&](int blk) __attribute__((always_inline)) {
+#pragma unroll
+    for (int p = 0; p < kPasses; ++p) {
+      const int pgi = blk * kBlockPages + p * kPagesPerPass + st_page;
+      const int id = clamp_page(pgi < row_pages ? bt[pgi] : bt[0], a.num_pages);
+      const size_t base = ((size_t)id * a.hkv + g) * head_stride;
+      kreg[p] = load_u32x4(a.k_pool + base + st_slot * kHeadDim + st_kch * 8);
+      vreg[p] = load_u32x4(a.v_pool + base + st_d * kPage + st_half * 8);
+    }
+  };
+  auto stage_store = [&](int blk, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int p = 0; p < kPasses; ++p) {
+      const int j = p * kPagesPerPass + st_page;        // page in the block
+      const int pos0 = (blk * kBlockPages + j) * kPage;
+      // V slots at or past the row's end may hold anything (NaN included):
+      // they are stored as zeros, so that a zero weight cannot meet a NaN in
+      // the P·V product. K slots there need nothing: every key at or past
+      // the row's end lies beyond the causal limit of every query, and its
+      // score is replaced by -inf (a select, not an arithmetic mask).
+      u32x4 vw = vreg[p];
+      if (pos0 + kPage > row_end) {
+        const int vpos = pos0 + st_half * 8;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = vpos + 2 * e < row_end ? 0xffffu : 0u;
+          const uint32_t hi = vpos + 2 * e + 1 < row_end ? 0xffff0000u : 0u;
+          vw[e] &= lo | hi;
+        }
+      }
+      *reinterpret_cast<u32x4 *>(&sK[buf * kKBlockElems + k_lds(j * kPage + st_slot, st_kch)]) =
+          kreg[p];
+      *reinterpret_cast<u32x4 *>(&sV[buf * kBlockElems + v_lds(j, st_d, st_half)]) = vw;
+    }
+  };
+
+  // ---- operand addressing. A row i of an S tile holds key pi(i): bits 2 and
+  // 3 of i swapped, so that lane l's value r is key 16 (r / 8) + 8 grp + r % 8.
+  const int ka_key = (col & ~12) | ((col & 4) << 1) | ((col & 8) >> 1);
+  // With a positive scale the scores stay raw and the scale is folded into
+  // the exponent's FMA; otherwise scores are scaled first.
+  const float c2 = a.scale_log2;
+  const float cs = kPosScale ? c2 : 1.f;
+
+  f32x16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;   // running max (scaled, base 2) and sum
+
+  stage_load(0);
+  stage_store(0, 0);
+  __syncthreads();
+
+  for (int blk = 0; blk < nblocks; ++blk) {
+    const int buf = blk & 1;
+    if (blk + 1 < nblocks) stage_load(blk + 1);
+    const uint16_t *kl = sK + buf * kKBlockElems;
+    const uint16_t *vl = sV + buf * kBlockElems;
+    const int key0 = blk * kBlock;
+    const bool need_mask = key0 + kBlock - 1 > wave_q0;
+
+    // S^T of pair pp: 32 keys (pages 2pp, 2pp + 1 of the block) x 32 query rows.
+    auto scores = [&](int pp) __attribute__((always_inline)) {
+      // all eight K operands are requested before the first product
+      const int krow = 32 * pp + ka_key;
+      bf16x8 ka[8];
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) ka[kk] = lds_bf16x8(&kl[k_lds(krow, 2 * kk + grp)]);
+      f32x16 st = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) st = mfma32x32x16(ka[kk], qop[kk], st);
+      return st;
+    };
+    // Online-softmax update and P·V of pair pp.
+    auto update = [&](int pp, f32x16 st) __attribute__((always_inline)) {
+      // V operands are requested first; their latency hides behind the softmax.
+      bf16x8 va[8];
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        va[2 * dt] = lds_bf16x8(&vl[v_lds(2 * pp, 32 * dt + col, grp)]);
+        va[2 * dt + 1] = lds_bf16x8(&vl[v_lds(2 * pp + 1, 32 * dt + col, grp)]);
+      }
+      float sc[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[r] = kPosScale ? st[r] : st[r] * c2;
+      if (need_mask) {
+        // value r is key key0 + 32 pp + 8 grp + 16 (r / 8) + r % 8; masked past qpos
+        const int rel = qpos - key0 - 32 * pp - 8 * grp;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] = 16 * (r >> 3) + (r & 7) > rel ? -INFINITY : sc[r];
+      }
+      // Weights against the running max m_run. It is only moved (and O, l
+      // rescaled) when some lane's weights sum past kSumLimit, or are not
+      // finite (the first pair, while m_run is still -inf); the weights are
+      // then recomputed against the new max. Between moves every weight
+      // stays below kSumLimit, which fp32 and bf16 carry without loss, and
+      // out = O / l does not depend on when the max moves.
+      f32x8 p0, p1;
+      bf16x8 pb0, pb1;
+      float psum;
+      // Weights, rounded to bf16 for the P·V product, and their sum taken
+      // from the rounded values (two chains of bf16 pair dot products with
+      // (1, 1)), so that l normalises exactly the weights O accumulates.
+      auto weights = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p0[e] = fast_exp2(__builtin_fmaf(sc[e], cs, -m_run));
+          p1[e] = fast_exp2(__builtin_fmaf(sc[8 + e], cs, -m_run));
+        }
+        pb0 = to_bf16x8(p0);
+        pb1 = to_bf16x8(p1);
+        const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+        float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s0 = __builtin_amdgcn_fdot2_f32_bf16(
+              bf16x2{pb0[2 * e], pb0[2 * e + 1]}, one, s0, false);
+          s1 = __builtin_amdgcn_fdot2_f32_bf16(
+              bf16x2{pb1[2 * e], pb1[2 * e + 1]}, one, s1, false);
+        }
+        psum = s0 + s1;
+      };
+      weights();
+      if (!__all(psum <= kSumLimit)) {
+        float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+#pragma unroll
+        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
+        mx = fmaxf(mx, sc[15]);
+        mx = pair_max(mx);
+        if (kPosScale) mx *= c2;
+        float m_new = fmaxf(m_run, mx);
+        if (m_new == -INFINITY) m_new = 0.f;   // nothing attended yet: any finite reference
+        const float alpha = fast_exp2(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
+        weights();
+      }
+      l_run += psum;
+      // O^T[d][qrow] += V^T[d][key] P^T[key][qrow]: page c of the pair, slots
+      // 8 grp + 0..7, d = 32 dt + col.
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        o[dt] = mfma32x32x16(va[2 * dt], pb0, o[dt]);
+        o[dt] = mfma32x32x16(va[2 * dt + 1], pb1, o[dt]);
+      }
+    };
+#pragma unroll
+    for (int pp = 0; pp < kBlock / 32; ++pp) update(pp, scores(pp));
+
+    if (blk + 1 < nblocks) stage_store(blk + 1, buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: normalise and store; lane holds d = 32 dt + 8 (r/4) + 4 grp + r%4 ----
+  const float l = l_run + __shfl_xor(l_run, 32);
+  if (qpos >= 0) {
+    const size_t row = (size_t)(cu0 + i0 + qi) * a.hq + (size_t)g * G + hh;
+    const float inv = 1.f / l;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[dt][4 * rq + e] * inv;
+        *reinterpret_cast<f32x4 *>(&a.out[row * kHeadDim + 32 * dt + 8 * rq + 4 * grp]) = v;
+      }
+    if (a.lse && grp == 0) a.lse[row] = (m_run + __log2f(l)) * kLn2;
+  }
+}
+
+// Kernel arguments of an append call (validated by the ABI layer).
+inline AppendArgs make_append_args(const uint16_t *q, const int32_t *cu_q,
+                                   const int32_t *ctx_lens, const PagedKV &kv, int32_t hq,
+                                   int32_t total_q, int32_t max_q_len, int32_t max_kv_len,
+                                   float scale, float *out, float *lse) {
+  AppendArgs a;
+  a.q = q;
+  a.k_pool = kv.k_pool;
+  a.v_pool = kv.v_pool;
+  a.block_table = kv.block_table;
+  a.cu_q = cu_q;
+  a.ctx_lens = ctx_lens;
+  a.out = out;
+  a.lse = lse;
+  a.hq = hq;
+  a.hkv = kv.hkv;
+  a.group = hq / kv.hkv;
+  a.bt_stride = kv.bt_stride;
+  a.num_pages = kv.num_pages;
+  a.total_q = total_q;
+  a.max_q_len = max_q_len;
+  a.max_kv_len = max_kv_len;
+  a.q_per_block = kRowsPerGroup / a.group;
+  a.scale_log2 = scale * kLog2e;
+  return a;
+}
+
+}  // namespace atile
+}  // namespace ra

@@ -55,6 +55,28 @@ hipError_t launch_append(const uint16_t *q, const int32_t *cu_q, const int32_t *
                          int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
                          float *lse, hipStream_t stream);
 
+// ---- mixed step: decode rows and append rows in one persistent launch ----
+// Workspace: a header, the append tile list, the decode split list and the
+// decode partial results, each at a 256-byte aligned offset.
+struct MixedLayout {
+  DecodePlan plan;            // decode splits
+  int32_t qblocks;            // query blocks of the longest append chunk
+  int64_t max_tiles;          // bound on append tile entries
+  int64_t max_splits;         // bound on decode split entries
+  size_t tiles_offset, splits_offset, partials_offset, bytes;
+};
+MixedLayout mixed_layout(int32_t B_decode, int32_t B_append, int32_t hq, int32_t hkv_decode,
+                         int32_t hkv_append, int32_t max_kv_len_decode, int32_t max_q_len);
+int32_t mixed_hkv_limit();   // KV heads an entry can name
+hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
+                        const int32_t *kv_lens, int32_t B_decode, int32_t max_kv_len_decode,
+                        float *out_decode, float *lse_decode, const uint16_t *q_append,
+                        const int32_t *cu_q, const int32_t *ctx_lens, const PagedKV &kv_append,
+                        int32_t B_append, int32_t total_q, int32_t max_q_len,
+                        int32_t max_kv_len_append, float *out_append, float *lse_append,
+                        int32_t hq, float scale, void *workspace, const MixedLayout &layout,
+                        hipStream_t stream);
+
 // ---- per-token log-probabilities under an LM head ----
 int32_t logprob_chunks(int32_t V);
 size_t logprob_workspace_bytes(int32_t N, int32_t V);

@@ -163,3 +163,49 @@ def test_page_write_and_gather_validation(lib):
     assert g(max_len=100) == _lib.RA_ERR_SHAPE
     assert g(kv=_kv(page_size=8)) == _lib.RA_ERR_UNSUPPORTED
     assert g(B=0) == _lib.RA_OK
+
+
+def _mixed(lib, kvd, kva, **kw):
+    d = dict(qd=FAKE, kv_lens=FAKE, Bd=2, mkd=64, outd=FAKE, lsed=None,
+             qa=FAKE, cu_q=FAKE, ctx=FAKE, Ba=2, total_q=10, mq=8, mka=64, outa=FAKE, lsea=None,
+             Hq=4, scale=0.1, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    d.update(kw)
+    return lib.rollout_attn_mixed(
+        d["qd"], None if kvd is None else ctypes.byref(kvd), d["kv_lens"], d["Bd"], d["mkd"],
+        d["outd"], d["lsed"], d["qa"], d["cu_q"], d["ctx"],
+        None if kva is None else ctypes.byref(kva), d["Ba"], d["total_q"], d["mq"], d["mka"],
+        d["outa"], d["lsea"], d["Hq"], d["scale"], d["ws"], d["ws_bytes"], d["stream"])
+
+
+def test_mixed_workspace_size(lib):
+    f = lib.rollout_attn_mixed_workspace_size
+    assert f(-1, 2, 32, 8, 8, 1000, 100) == 0
+    assert f(4, 4, 30, 8, 8, 1000, 100) == 0             # Hq % Hkv
+    a = f(64, 8, 32, 8, 8, 32768, 2048)
+    # at least the decode partials, plus the work lists
+    assert a > lib.rollout_attn_decode_workspace_size(64, 32, 8, 32768)
+    assert f(64, 8, 32, 8, 8, 32768, 4096) > a            # more query blocks, longer tile list
+    assert f(0, 8, 32, 8, 8, 0, 2048) > 0                 # append only
+    assert f(64, 0, 32, 8, 8, 32768, 0) > 0               # decode only
+
+
+def test_mixed_validation(lib):
+    kv = _kv()
+    assert _mixed(lib, kv, kv, qd=None) == _lib.RA_ERR_NULL
+    assert _mixed(lib, kv, kv, cu_q=None) == _lib.RA_ERR_NULL
+    assert _mixed(lib, None, kv) == _lib.RA_ERR_NULL
+    assert _mixed(lib, kv, None) == _lib.RA_ERR_NULL
+    assert _mixed(lib, kv, kv, Bd=-1) == _lib.RA_ERR_SHAPE
+    assert _mixed(lib, kv, kv, total_q=-1) == _lib.RA_ERR_SHAPE
+    assert _mixed(lib, kv, kv, Hq=3) == _lib.RA_ERR_SHAPE                # Hq % Hkv
+    assert _mixed(lib, kv, kv, mkd=65) == _lib.RA_ERR_SHAPE              # > bt_stride * 16
+    assert _mixed(lib, kv, kv, mq=65, mka=64) == _lib.RA_ERR_SHAPE       # chunk > max_kv_len
+    assert _mixed(lib, kv, kv, Hq=34) == _lib.RA_ERR_UNSUPPORTED         # decode group of 17
+    assert _mixed(lib, kv, _kv(page_size=32)) == _lib.RA_ERR_UNSUPPORTED
+    assert _mixed(lib, kv, _kv(num_kv_heads=512, num_pages=10), Hq=512,
+                  Bd=0) == _lib.RA_ERR_UNSUPPORTED                       # > 256 KV heads
+    assert _mixed(lib, kv, kv, ws_bytes=16) == _lib.RA_ERR_WORKSPACE
+    assert _mixed(lib, kv, kv, ws=None) == _lib.RA_ERR_WORKSPACE
+    # an empty side is not checked at all; both empty: no work, no launch
+    assert _mixed(lib, None, None, Bd=0, Ba=0, qd=None, qa=None) == _lib.RA_OK
+    assert _mixed(lib, kv, None, Bd=0, total_q=0, ws=None) == _lib.RA_OK
