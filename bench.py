@@ -64,8 +64,12 @@ def write_bytes(n_new: int, Hkv: int, D: int = 128) -> int:
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = {
-    "decode": ("paper_2603_18815_amd/csrc/ra_decode.hip", "paper_2603_18815_amd/csrc/ra_device.h"),
-    "append": ("paper_2603_18815_amd/csrc/ra_append.hip", "paper_2603_18815_amd/csrc/ra_device.h"),
+    "decode": ("paper_2603_18815_amd/csrc/ra_decode.hip",
+               "paper_2603_18815_amd/csrc/ra_decode_split.h",
+               "paper_2603_18815_amd/csrc/ra_device.h"),
+    "append": ("paper_2603_18815_amd/csrc/ra_persistent.hip",
+               "paper_2603_18815_amd/csrc/ra_append_tile.h",
+               "paper_2603_18815_amd/csrc/ra_device.h"),
 }
 TRAFFIC_FILES = {
     "decode": "profiles/decode_qwen3_8b_b64.hbm_traffic.txt",
@@ -172,6 +176,8 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
     out_a = torch.empty((int(w.q_lens.sum()), w.Hq, 128), dtype=torch.float32, device=dev)
     ws = torch.empty(ra.decode_workspace_size(w.kv_lens.shape[0], w.Hq, w.Hkv, max_kv_d),
                      dtype=torch.uint8, device=dev)
+    ws_a = torch.empty(ra.append_workspace_size(w.q_lens.shape[0], w.Hq, w.Hkv, max_q),
+                       dtype=torch.uint8, device=dev)
 
     def step(ev=None):
         if ev is not None:
@@ -182,7 +188,8 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
         ra.decode(t.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
         if ev is not None:
             ev[2].record()
-        ra.append(t.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a)
+        ra.append(t.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a,
+                  workspace=ws_a)
         if ev is not None:
             ev[3].record()
 
@@ -247,7 +254,7 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
             "frac_of_overlap_bound": round(ovl_ms / single_ms, 4),
         },
     }
-    del t, out_d, out_a, ws, ws_mix
+    del t, out_d, out_a, ws, ws_a, ws_mix
     torch.cuda.empty_cache()
     return res
 
@@ -417,6 +424,8 @@ def main():
     out_a = torch.empty((int(wa.q_lens.sum()), wa.Hq, 128), dtype=torch.float32, device=dev)
     ws = torch.empty(ra.decode_workspace_size(wd.kv_lens.shape[0], wd.Hq, wd.Hkv, max_kv_d),
                      dtype=torch.uint8, device=dev)
+    ws_a = torch.empty(ra.append_workspace_size(wa.q_lens.shape[0], wa.Hq, wa.Hkv, max_q),
+                       dtype=torch.uint8, device=dev)
     max_new_d, max_pos_d = 1, max_kv_d
     max_new_a, max_pos_a = max_q, max_kv_a
 
@@ -430,7 +439,8 @@ def main():
         ra.decode(td.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
         if ev is not None:
             ev[2].record()
-        ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a)
+        ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a,
+                  workspace=ws_a)
         if ev is not None:
             ev[3].record()
 
@@ -448,7 +458,7 @@ def main():
                     "decode": lambda: ra.decode(td.q_decode, kv_d, kv_lens, max_kv_d, SCALE,
                                                 out=out_d, workspace=ws),
                     "append": lambda: ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv_a,
-                                                SCALE, out=out_a)}[args.only]
+                                                SCALE, out=out_a, workspace=ws_a)}[args.only]
         for _ in range(args.warmup + args.steps):
             part()
         torch.cuda.synchronize()
@@ -528,7 +538,8 @@ def main():
                      "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic("decode")},
-        "roofline_append": {"kernel": "append_kernel", "bound": "mfma",
+        "roofline_append": {"kernel": "rollout_attn_append (mixed_plan_kernel + mixed_kernel)",
+                            "bound": "mfma",
                             "achieved": round(app_tfs, 1), "peak": BF16_PEAK_TFLOPS,
                             "unit": "TFLOP/s", "frac": round(app_tfs / BF16_PEAK_TFLOPS, 4),
                             "traffic": measured_traffic("append")},

@@ -181,19 +181,29 @@ int rollout_attn_decode_shared_prefix(const void *q, const ra_paged_kv *kv,
  *   max_kv_len  host: an upper bound of ctx_lens[b] + T_b; <= bt_stride * 16
  *   out         fp32 [total_q][Hq][128]
  *   lse         fp32 [total_q][Hq] or NULL
- * Needs no workspace. Errors as for decode.
+ *   workspace   device scratch of at least
+ *               rollout_attn_append_workspace_size(B, Hq, Hkv, max_q_len) bytes
+ *               (the call's work list and counter, rewritten by every call;
+ *               contents on entry are ignored). Calls that share a workspace
+ *               must not overlap.
+ * The work is planned on the device (a one-workgroup kernel sorts the tiles
+ * by length, longest first) and run by one persistent workgroup per CU.
+ * Errors as for decode; RA_ERR_UNSUPPORTED also for more than 256 KV heads.
  */
+size_t rollout_attn_append_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
+                                          int32_t max_q_len);
 int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_lens,
                         const ra_paged_kv *kv, int32_t B, int32_t Hq, int32_t total_q,
                         int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
-                        float *lse, hipStream_t stream);
+                        float *lse, void *workspace, size_t workspace_bytes,
+                        hipStream_t stream);
 
 /*
  * Mixed step: the attention of one rollout step in which some trajectories
  * decode a token while others have just had tool observations appended
  * (Sec. 3.3.1: many rollout workers drive their agent loops concurrently, each
  * firing LLM calls; Sec. 3.3.3: observations are appended to the retained
- * tokens). Computes, in one persistent launch over the GPU (plus a one-
+ * tokens). Computes, in one persistent launch over the GPU (plus the one-
  * workgroup planning kernel before it and the decode combine after it):
  *   - for the decode rows, exactly what rollout_attn_decode computes
  *     (up to rounding: each split is summed by twice as many waves);

@@ -25,7 +25,7 @@ HEAD_DIM = 128
 
 __all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "mixed", "kv_page_write",
            "kv_page_gather", "token_logprob", "decode_workspace_size",
-           "decode_shared_prefix_workspace_size", "mixed_workspace_size",
+           "decode_shared_prefix_workspace_size", "append_workspace_size", "mixed_workspace_size",
            "token_logprob_workspace_size", "abi_version", "RolloutAttnError"]
 
 
@@ -194,7 +194,8 @@ def decode_shared_prefix(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor,
 def append(q: torch.Tensor, cu_q: torch.Tensor, ctx_lens: torch.Tensor, kv: PagedKV,
            max_q_len: Optional[int] = None, max_kv_len: Optional[int] = None,
            scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
-           lse: Optional[torch.Tensor] = None, want_lse: bool = False, stream=None
+           lse: Optional[torch.Tensor] = None, want_lse: bool = False,
+           workspace: Optional[torch.Tensor] = None, stream=None
            ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
     """Append attention; q bf16 [total_q][Hq][128] -> out fp32 [total_q][Hq][128]."""
     lib = _lib.load()
@@ -224,11 +225,20 @@ def append(q: torch.Tensor, cu_q: torch.Tensor, ctx_lens: torch.Tensor, kv: Page
     if lse is not None:
         _need(lse, "lse", torch.float32, dev)
         _shape(lse, (total_q, Hq), "lse")
+    ws_bytes = lib.rollout_attn_append_workspace_size(B, Hq, kv.num_kv_heads, max_q_len)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    _need(workspace, "workspace", torch.uint8, dev)
     s = kv.struct()
     _lib.check("rollout_attn_append", lib.rollout_attn_append(
         q.data_ptr(), cu_q.data_ptr(), ctx_lens.data_ptr(), ctypes.byref(s), B, Hq, total_q,
-        max_q_len, max_kv_len, float(scale), out.data_ptr(), _ptr(lse), _stream(dev, stream)))
+        max_q_len, max_kv_len, float(scale), out.data_ptr(), _ptr(lse), workspace.data_ptr(),
+        workspace.numel(), _stream(dev, stream)))
     return out, lse
+
+
+def append_workspace_size(B: int, Hq: int, Hkv: int, max_q_len: int) -> int:
+    return int(_lib.load().rollout_attn_append_workspace_size(B, Hq, Hkv, max_q_len))
 
 
 def mixed_workspace_size(B_decode: int, B_append: int, Hq: int, Hkv_decode: int,

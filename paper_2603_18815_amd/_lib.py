@@ -19,6 +19,7 @@ EXPORTS = (
     "rollout_attn_decode",
     "rollout_attn_decode_shared_prefix_workspace_size",
     "rollout_attn_decode_shared_prefix",
+    "rollout_attn_append_workspace_size",
     "rollout_attn_append",
     "rollout_attn_mixed_workspace_size",
     "rollout_attn_mixed",
@@ -76,8 +77,10 @@ def load() -> ctypes.CDLL:
     lib.rollout_attn_decode_shared_prefix.argtypes = [vp, kvp, vp, vp, vp, i32, i32, i32, i32,
                                                       i32, i32, f32, vp, vp, vp, sz, vp]
     lib.rollout_attn_decode_shared_prefix.restype = ctypes.c_int
+    lib.rollout_attn_append_workspace_size.argtypes = [i32, i32, i32, i32]
+    lib.rollout_attn_append_workspace_size.restype = sz
     lib.rollout_attn_append.argtypes = [vp, vp, vp, kvp, i32, i32, i32, i32, i32, f32, vp, vp,
-                                        vp]
+                                        vp, sz, vp]
     lib.rollout_attn_append.restype = ctypes.c_int
     lib.rollout_attn_mixed_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
     lib.rollout_attn_mixed_workspace_size.restype = sz

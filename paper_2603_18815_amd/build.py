@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "librollout_attn.so")
-SOURCES = ["ra_api.hip", "ra_page.hip", "ra_decode.hip", "ra_append.hip", "ra_mixed.hip",
+SOURCES = ["ra_api.hip", "ra_page.hip", "ra_decode.hip", "ra_persistent.hip",
            "ra_logprob.hip"]
 ARCH = "gfx950"
 

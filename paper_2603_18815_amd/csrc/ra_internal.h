@@ -49,15 +49,10 @@ hipError_t launch_decode_shared_prefix(const uint16_t *q, const PagedKV &kv,
                                        float *out, float *lse, void *workspace,
                                        const DecodePlan &plan, hipStream_t stream);
 
-// ---- append (causal chunked prefill against the cache) ----
-hipError_t launch_append(const uint16_t *q, const int32_t *cu_q, const int32_t *ctx_lens,
-                         const PagedKV &kv, int32_t B, int32_t hq, int32_t total_q,
-                         int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
-                         float *lse, hipStream_t stream);
-
-// ---- mixed step: decode rows and append rows in one persistent launch ----
-// Workspace: a header, the append tile list, the decode split list and the
-// decode partial results, each at a 256-byte aligned offset.
+// ---- append, and the mixed step (decode rows and append rows), in one
+// planned persistent launch; append alone is the mixed step without decode
+// rows. Workspace: a header, the append tile list, the decode split list and
+// the decode partial results, each at a 256-byte aligned offset.
 struct MixedLayout {
   DecodePlan plan;            // decode splits
   int32_t qblocks;            // query blocks of the longest append chunk

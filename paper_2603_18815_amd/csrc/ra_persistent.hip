@@ -1,13 +1,13 @@
-// One rollout step's attention in a single persistent launch: decode rows
-// (one new token each) and append rows (a chunk of new observation tokens
-// each) against their paged caches.
+// Planned persistent launches: append rows alone, or one rollout step's
+// decode rows (one new token each) and append rows (a chunk of new
+// observation tokens each) together, against their paged caches.
 //
 // A plan kernel (one workgroup) lists the work of the call from the
 // device-resident lengths:
 //   - append tiles (row, query block, KV head), sorted by the number of
 //     64-key blocks they walk, longest first (a counting sort over the key
 //     block counts), so that the long tiles start early and the short ones
-//     fill the end;
+//     fill the end instead of leaving CUs idle behind one long tile;
 //   - decode splits (row, split, KV head), row by row.
 // The attention kernel then runs one workgroup of 8 waves per CU; each
 // workgroup takes the next entry of one merged order from a device counter
@@ -19,10 +19,9 @@
 // j of the merged order (n entries, nd of them decode splits) is decode
 // split floor(j nd / n) when floor((j + 1) nd / n) > floor(j nd / n), else
 // append tile j - floor(j nd / n).
-// An append tile is computed exactly as by the append kernel; a decode split
-// as by the decode split kernel but with 8 waves; the decode combine follows
-// as in plain decode. Results do not depend on the order in which entries
-// are taken.
+// A decode split is computed as by the decode split kernel but with 8 waves;
+// the decode combine follows as in plain decode. Results do not depend on
+// the order in which entries are taken.
 #include "ra_append_tile.h"
 #include "ra_decode_split.h"
 #include "ra_internal.h"
@@ -127,7 +126,8 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m) {
   }
 }
 
-template <bool kPosScale>
+// kDecode: the call has decode rows (otherwise every entry is an append tile).
+template <bool kPosScale, bool kDecode>
 __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
   __shared__ union {
     atile::AppendLds ap;
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
     const int j = __builtin_amdgcn_readfirstlane(s_next);
     if (j >= n) break;
     const int dj = (int)((int64_t)j * nd / n);
-    if ((int)(((int64_t)j + 1) * nd / n) > dj) {
+    if (kDecode && (int)(((int64_t)j + 1) * nd / n) > dj) {
       const int2 e = m.splits[dj];
       dsplit::decode_split<1, false, kMixWaves>(m.de, e.y & ((1 << kHeadBits) - 1),
                                                 e.y >> kHeadBits, e.x, lds.de);
@@ -211,10 +211,19 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
     return e;
   const int64_t entries = layout.max_tiles + layout.max_splits;
   const unsigned grid = (unsigned)(entries < cus ? (entries > 0 ? entries : 1) : cus);
-  if (m.ap.scale_log2 > 0.f || B_append == 0)
-    hipLaunchKernelGGL(mixed_kernel<true>, dim3(grid), dim3(kMixThreads), 0, stream, m);
-  else
-    hipLaunchKernelGGL(mixed_kernel<false>, dim3(grid), dim3(kMixThreads), 0, stream, m);
+  const dim3 g(grid), b(kMixThreads);
+  const bool pos = m.ap.scale_log2 > 0.f || B_append == 0;
+  if (B_decode == 0) {
+    if (pos)
+      hipLaunchKernelGGL((mixed_kernel<true, false>), g, b, 0, stream, m);
+    else
+      hipLaunchKernelGGL((mixed_kernel<false, false>), g, b, 0, stream, m);
+  } else {
+    if (pos)
+      hipLaunchKernelGGL((mixed_kernel<true, true>), g, b, 0, stream, m);
+    else
+      hipLaunchKernelGGL((mixed_kernel<false, true>), g, b, 0, stream, m);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (B_decode == 0) return hipSuccess;
   hipLaunchKernelGGL(dsplit::decode_combine_kernel, dim3(hq, B_decode), dim3(kHeadDim), 0, stream,

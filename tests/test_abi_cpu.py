@@ -131,19 +131,32 @@ def test_token_logprob_validation(lib):
 def test_append_validation(lib):
     def call(kv, **kw):
         d = dict(q=FAKE, cu=FAKE, ctx=FAKE, B=2, Hq=4, total_q=10, max_q=5, max_kv=64,
-                 out=FAKE)
+                 out=FAKE, ws=FAKE, ws_bytes=1 << 30)
         d.update(kw)
         return lib.rollout_attn_append(d["q"], d["cu"], d["ctx"], ctypes.byref(kv), d["B"],
                                        d["Hq"], d["total_q"], d["max_q"], d["max_kv"], 0.1,
-                                       d["out"], None, None)
+                                       d["out"], None, d["ws"], d["ws_bytes"], None)
     assert call(_kv(), cu=None) == _lib.RA_ERR_NULL
     assert call(_kv(), total_q=-1) == _lib.RA_ERR_SHAPE
     assert call(_kv(), max_kv=100) == _lib.RA_ERR_SHAPE
     assert call(_kv(), max_q=70, max_kv=64) == _lib.RA_ERR_SHAPE
     assert call(_kv(), Hq=5) == _lib.RA_ERR_SHAPE
     assert call(_kv(head_dim=256)) == _lib.RA_ERR_UNSUPPORTED
-    assert call(_kv(), total_q=0) == _lib.RA_OK
-    assert call(_kv(), B=0) == _lib.RA_OK
+    assert call(_kv(), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
+    assert call(_kv(), ws=None) == _lib.RA_ERR_WORKSPACE
+    assert call(_kv(num_kv_heads=512), Hq=512) == _lib.RA_ERR_UNSUPPORTED   # > 256 KV heads
+    assert call(_kv(), total_q=0, ws=None) == _lib.RA_OK                   # no work, no launch
+    assert call(_kv(), B=0, ws=None) == _lib.RA_OK
+
+
+def test_append_workspace_size(lib):
+    f = lib.rollout_attn_append_workspace_size
+    assert f(0, 32, 8, 100) == 0
+    assert f(4, 30, 8, 100) == 0                                  # Hq % Hkv
+    a = f(32, 32, 8, 2048)
+    assert a >= 32 * (2048 // 64) * 8 * 8                         # one 8-byte entry per tile
+    assert f(32, 32, 8, 4096) > a
+    assert f(32, 32, 8, 2048) == lib.rollout_attn_mixed_workspace_size(0, 32, 32, 8, 8, 0, 2048)
 
 
 def test_page_write_and_gather_validation(lib):
