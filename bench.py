@@ -384,10 +384,11 @@ def main():
                     help="skip the token log-probability leg (Qwen3-8B LM head)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-step leg (B = 512, 85 %% decode / 15 %% append rows)")
-    ap.add_argument("--only", choices=["write", "decode", "append", "copy"],
+    ap.add_argument("--only", choices=["write", "decode", "append", "copy", "mixed"],
                     help="run only this part of the step --steps times after --warmup "
-                         "(for rocprofv3 counter runs; 'copy' is a 1 GiB torch copy used to "
-                         "calibrate the HBM byte counters); prints no JSON line")
+                         "(for rocprofv3 runs; 'copy' is a 1 GiB torch copy used to "
+                         "calibrate the HBM byte counters, 'mixed' the mixed-step leg); "
+                         "prints no JSON line")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -402,6 +403,10 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only == "mixed":
+        res = mixed_step(ra, synth, dev, args.steps, args.warmup)
+        print(f"[bench] mixed step {json.dumps(res)}", flush=True)
+        return
     wd, wa = synth.config(2), synth.config(3)
     td, ta = synth.make_tensors(wd, dev), synth.make_tensors(wa, dev)
 

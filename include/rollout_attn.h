@@ -186,8 +186,9 @@ int rollout_attn_decode_shared_prefix(const void *q, const ra_paged_kv *kv,
  *               (the call's work list and counter, rewritten by every call;
  *               contents on entry are ignored). Calls that share a workspace
  *               must not overlap.
- * The work is planned on the device (a one-workgroup kernel sorts the tiles
- * by length, longest first) and run by one persistent workgroup per CU.
+ * The work is planned on the device (a one-workgroup kernel orders the rows
+ * longest first and queues each KV head's tiles for one XCD) and run by one
+ * persistent workgroup per CU.
  * Errors as for decode; RA_ERR_UNSUPPORTED also for more than 256 KV heads.
  */
 size_t rollout_attn_append_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
@@ -209,7 +210,7 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
  *     (up to rounding: each split is summed by twice as many waves);
  *   - for the append rows, bitwise what rollout_attn_append computes.
  * Append tiles are taken longest first and the decode splits are spread
- * among them, so that decode's HBM traffic overlaps append's matrix work.
+ * among them, so that decode's HBM traffic can overlap append's matrix work.
  * The two sides may use different block tables (and pools); either side may
  * be empty (B_decode == 0, or B_append == 0 / total_q == 0 / max_q_len == 0),
  * in which case its pointers are not used and may be NULL.

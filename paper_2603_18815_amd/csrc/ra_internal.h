@@ -51,8 +51,9 @@ hipError_t launch_decode_shared_prefix(const uint16_t *q, const PagedKV &kv,
 
 // ---- append, and the mixed step (decode rows and append rows), in one
 // planned persistent launch; append alone is the mixed step without decode
-// rows. Workspace: a header, the append tile list, the decode split list and
-// the decode partial results, each at a 256-byte aligned offset.
+// rows. Workspace: a header, the append row order, the append tile list, the
+// decode split list and the decode partial results, each at a 256-byte
+// aligned offset.
 struct MixedLayout {
   DecodePlan plan;            // decode splits
   int32_t qblocks;            // query blocks of the longest append chunk

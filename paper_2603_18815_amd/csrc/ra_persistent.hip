@@ -3,22 +3,26 @@
 // observation tokens each) together, against their paged caches.
 //
 // A plan kernel (one workgroup) lists the work of the call from the
-// device-resident lengths:
-//   - append tiles (row, query block, KV head), sorted by the number of
-//     64-key blocks they walk, longest first (a counting sort over the key
-//     block counts), so that the long tiles start early and the short ones
-//     fill the end instead of leaving CUs idle behind one long tile;
+// device-resident lengths, in one queue per XCD; queue q takes KV heads
+// q, q + 8, q + 16, ...:
+//   - append tiles (row, query block, KV head): the rows sorted by the key
+//     blocks of their longest (last) tile, longest first (a counting sort),
+//     each row's query blocks last first. The long tiles start early and the
+//     short ones fill the end, and the tiles of one row and head follow each
+//     other, so that the CUs of an XCD walk the same pages of K/V at about
+//     the same time and share them through the XCD's L2;
 //   - decode splits (row, split, KV head), row by row.
-// The attention kernel then runs one workgroup of 8 waves per CU; each
-// workgroup takes the next entry of one merged order from a device counter
-// until the order is used up. The merged order places the decode splits at
-// even spacing among the append tiles, so that at any time a few CUs stream
-// KV pages for decode (bound by HBM) while the rest run the append tiles'
-// matrix products (bound by the matrix cores): the decode bytes are read
-// while the matrix cores are busy instead of in a phase of their own. Entry
-// j of the merged order (n entries, nd of them decode splits) is decode
-// split floor(j nd / n) when floor((j + 1) nd / n) > floor(j nd / n), else
-// append tile j - floor(j nd / n).
+// The attention kernel then runs one workgroup of 8 waves per CU. Workgroups
+// are placed on the XCDs round robin, so workgroup w starts on queue w mod 8
+// and, once that queue is used up, takes what is left in the others. In each
+// queue the workgroups take the next entry of one merged order from a device
+// counter. The merged order places the decode splits at even spacing among
+// the append tiles, so that a few CUs stream KV pages for decode (bound by
+// HBM) while the rest run the append tiles' matrix products (bound by the
+// matrix cores). Entry j of a queue's merged order (n entries, nd of them
+// decode splits) is decode split floor(j nd / n) when
+// floor((j + 1) nd / n) > floor(j nd / n), else append tile
+// j - floor(j nd / n).
 // A decode split is computed as by the decode split kernel but with 8 waves;
 // the decode combine follows as in plain decode. Results do not depend on
 // the order in which entries are taken.
@@ -35,13 +39,16 @@ static_assert(kMixThreads == atile::kThreads, "append tiles take the whole workg
 constexpr int kPlanThreads = 1024;
 constexpr int kCostBuckets = 4096;   // key-block counts above this share the last bucket
 constexpr int kHeadBits = 8;         // entry = {row, index << kHeadBits | KV head}
+constexpr int kQueues = 8;           // one work queue per XCD
 
 struct MixedArgs {
   atile::AppendArgs ap;
   dsplit::DecodeArgs de;
-  int2 *tiles;      // append tiles, longest first
-  int2 *splits;     // decode splits
-  int32_t *header;  // [0] next merged entry, [1] append tiles, [2] decode splits
+  int2 *tiles;      // append tiles, one segment per queue
+  int2 *splits;     // decode splits, one segment per queue
+  int32_t *order;   // append rows, longest chunk end first
+  int32_t *header;  // per queue q: [q] next entry, [8+q] tiles, [16+q] splits,
+                    // [24+q] tile segment start, [32+q] split segment start
   int32_t B_append, qblocks;
 };
 
@@ -63,25 +70,38 @@ __device__ int block_exclusive_scan(int v, int *s, int *total) {
   return incl - v;
 }
 
+// KV heads g = q, q + 8, ... below hkv go to queue q.
+__device__ __forceinline__ int heads_of_queue(int hkv, int q) {
+  return q < hkv ? (hkv - 1 - q) / kQueues + 1 : 0;
+}
+
+// Query blocks of row b with work (0 for an empty row).
+__device__ __forceinline__ int row_qblocks(const atile::AppendArgs &ap, const atile::AppendRow &r) {
+  if (r.T <= 0 || r.ctx < 0) return 0;
+  return (r.T + ap.q_per_block - 1) / ap.q_per_block;
+}
+
 __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m) {
-  __shared__ int count[kCostBuckets];   // tiles per key-block count, then write cursors
+  __shared__ int count[kCostBuckets];   // rows per key-block count, then write cursors
   __shared__ int s_scan[kPlanThreads];
+  __shared__ int s_total;
   const int tid = threadIdx.x;
   const int hkv_a = m.ap.hkv, hkv_d = m.de.hkv;
   for (int c = tid; c < kCostBuckets; c += kPlanThreads) count[c] = 0;
+  if (tid == 0) s_total = 0;
   __syncthreads();
 
-  // ---- append tiles: bucket c holds the (row, query block) pairs that walk
-  // c + 1 key blocks (or more, in the last bucket)
-  const int pairs = m.B_append * m.qblocks;
-  for (int i = tid; i < pairs; i += kPlanThreads) {
-    const int b = i / m.qblocks, qb = i - b * m.qblocks;
-    const int nb = atile::append_tile_blocks(m.ap, atile::append_row(m.ap, b), qb);
-    if (nb > 0) atomicAdd(&count[min(nb, kCostBuckets) - 1], 1);
+  // ---- append rows, by the key blocks of their longest (last) tile, longest first
+  for (int b = tid; b < m.B_append; b += kPlanThreads) {
+    const atile::AppendRow r = atile::append_row(m.ap, b);
+    const int nq = row_qblocks(m.ap, r);
+    if (nq == 0) continue;
+    const int nb = atile::append_tile_blocks(m.ap, r, nq - 1);
+    atomicAdd(&count[min(nb, kCostBuckets) - 1], 1);
+    atomicAdd(&s_total, nq);
   }
   __syncthreads();
-  // cursors: bucket c starts after every bucket above it (longest first);
-  // thread t owns buckets kCostBuckets - 1 - (kPer t + k), k < kPer
+  const int total_nq = s_total;
   constexpr int kPer = kCostBuckets / kPlanThreads;
   int own[kPer], sum = 0;
 #pragma unroll
@@ -89,40 +109,85 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m) {
     own[k] = count[kCostBuckets - 1 - (kPer * tid + k)];
     sum += own[k];
   }
-  int n_pairs;
-  int cursor = block_exclusive_scan(sum, s_scan, &n_pairs);
+  int n_rows;
+  int cursor = block_exclusive_scan(sum, s_scan, &n_rows);
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
     count[kCostBuckets - 1 - (kPer * tid + k)] = cursor;
     cursor += own[k];
   }
   __syncthreads();
-  for (int i = tid; i < pairs; i += kPlanThreads) {
-    const int b = i / m.qblocks, qb = i - b * m.qblocks;
-    const int nb = atile::append_tile_blocks(m.ap, atile::append_row(m.ap, b), qb);
-    if (nb <= 0) continue;
-    const int p = atomicAdd(&count[min(nb, kCostBuckets) - 1], 1);
-    for (int g = 0; g < hkv_a; ++g)
-      m.tiles[(size_t)p * hkv_a + g] = make_int2(b, qb << kHeadBits | g);
+  for (int b = tid; b < m.B_append; b += kPlanThreads) {
+    const atile::AppendRow r = atile::append_row(m.ap, b);
+    const int nq = row_qblocks(m.ap, r);
+    if (nq == 0) continue;
+    const int nb = atile::append_tile_blocks(m.ap, r, nq - 1);
+    m.order[atomicAdd(&count[min(nb, kCostBuckets) - 1], 1)] = b;
+  }
+  __syncthreads();
+  // ---- tiles: queue q holds heads q, q + 8, ...; in it, rows in the order
+  // above, each row's query blocks last first, then its heads
+  int seg_a[kQueues], acc = 0;
+#pragma unroll
+  for (int q = 0; q < kQueues; ++q) {
+    seg_a[q] = acc;
+    acc += heads_of_queue(hkv_a, q) * total_nq;
+  }
+  int done = 0;   // query blocks of the rows ranked before this chunk
+  for (int k0 = 0; k0 < n_rows; k0 += kPlanThreads) {
+    const int k = k0 + tid;
+    const int b = k < n_rows ? m.order[k] : 0;
+    const int nq = k < n_rows ? row_qblocks(m.ap, atile::append_row(m.ap, b)) : 0;
+    int chunk;
+    const int before = done + block_exclusive_scan(nq, s_scan, &chunk);
+    for (int i = 0; i < nq; ++i) {
+      const int qb = nq - 1 - i;
+      for (int g = 0; g < hkv_a; ++g) {
+        const int q = g % kQueues, hq = heads_of_queue(hkv_a, q);
+        m.tiles[(size_t)seg_a[q] + (size_t)(before + i) * hq + g / kQueues] =
+            make_int2(b, qb << kHeadBits | g);
+      }
+    }
+    done += chunk;
   }
 
-  // ---- decode splits, row by row, KV head fastest
+  // ---- decode splits: queue q holds heads q, q + 8, ...; rows in order
+  int total_ns = 0;
   const int S = m.de.split_tokens;
-  int n_split_rows = 0;   // (row, split) pairs listed so far
   for (int r0 = 0; r0 < m.de.B; r0 += kPlanThreads) {
     const int b = r0 + tid;
     const int ns = b < m.de.B ? (dsplit::row_len(m.de, b) + S - 1) / S : 0;
-    int chunk_total;
-    const int first = n_split_rows + block_exclusive_scan(ns, s_scan, &chunk_total);
-    for (int s = 0; s < ns; ++s)
-      for (int g = 0; g < hkv_d; ++g)
-        m.splits[(size_t)(first + s) * hkv_d + g] = make_int2(b, s << kHeadBits | g);
-    n_split_rows += chunk_total;
+    int chunk;
+    block_exclusive_scan(ns, s_scan, &chunk);
+    total_ns += chunk;
   }
-  if (tid == 0) {
-    m.header[0] = 0;
-    m.header[1] = n_pairs * hkv_a;
-    m.header[2] = n_split_rows * hkv_d;
+  int seg_d[kQueues];
+  acc = 0;
+#pragma unroll
+  for (int q = 0; q < kQueues; ++q) {
+    seg_d[q] = acc;
+    acc += heads_of_queue(hkv_d, q) * total_ns;
+  }
+  done = 0;
+  for (int r0 = 0; r0 < m.de.B; r0 += kPlanThreads) {
+    const int b = r0 + tid;
+    const int ns = b < m.de.B ? (dsplit::row_len(m.de, b) + S - 1) / S : 0;
+    int chunk;
+    const int before = done + block_exclusive_scan(ns, s_scan, &chunk);
+    for (int s = 0; s < ns; ++s)
+      for (int g = 0; g < hkv_d; ++g) {
+        const int q = g % kQueues, hq = heads_of_queue(hkv_d, q);
+        m.splits[(size_t)seg_d[q] + (size_t)(before + s) * hq + g / kQueues] =
+            make_int2(b, s << kHeadBits | g);
+      }
+    done += chunk;
+  }
+  if (tid < kQueues) {
+    m.header[tid] = 0;
+    m.header[8 + tid] = heads_of_queue(hkv_a, tid) * total_nq;
+    m.header[16 + tid] = heads_of_queue(hkv_d, tid) * total_ns;
+    m.header[24 + tid] = seg_a[tid];
+    m.header[32 + tid] = seg_d[tid];
   }
 }
 
@@ -134,23 +199,31 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
     dsplit::DecodeLds<1, kMixWaves> de;
   } lds;
   __shared__ int s_next;
-  const int na = m.header[1], nd = m.header[2];
-  const int64_t n = (int64_t)na + nd;
-  for (;;) {
-    __syncthreads();   // the previous entry is done with LDS and s_next
-    if (threadIdx.x == 0) s_next = atomicAdd(&m.header[0], 1);
-    __syncthreads();
-    const int j = __builtin_amdgcn_readfirstlane(s_next);
-    if (j >= n) break;
-    const int dj = (int)((int64_t)j * nd / n);
-    if (kDecode && (int)(((int64_t)j + 1) * nd / n) > dj) {
-      const int2 e = m.splits[dj];
-      dsplit::decode_split<1, false, kMixWaves>(m.de, e.y & ((1 << kHeadBits) - 1),
-                                                e.y >> kHeadBits, e.x, lds.de);
-    } else {
-      const int2 e = m.tiles[j - dj];
-      atile::append_tile<kPosScale>(m.ap, e.y >> kHeadBits, e.y & ((1 << kHeadBits) - 1), e.x,
-                                    lds.ap);
+  // workgroups are placed on the XCDs round robin: start with this XCD's
+  // queue, then take what is left in the others
+  const int x = blockIdx.x % kQueues;
+  for (int qi = 0; qi < kQueues; ++qi) {
+    const int q = (x + qi) % kQueues;
+    const int na = m.header[8 + q], nd = m.header[16 + q];
+    const int64_t n = (int64_t)na + nd;
+    const int2 *tiles = m.tiles + m.header[24 + q];
+    const int2 *splits = m.splits + m.header[32 + q];
+    for (;;) {
+      __syncthreads();   // the previous entry is done with LDS and s_next
+      if (threadIdx.x == 0) s_next = n > 0 ? atomicAdd(&m.header[q], 1) : 0;
+      __syncthreads();
+      const int j = __builtin_amdgcn_readfirstlane(s_next);
+      if (j >= n) break;
+      const int dj = (int)((int64_t)j * nd / n);
+      if (kDecode && (int)(((int64_t)j + 1) * nd / n) > dj) {
+        const int2 e = splits[dj];
+        dsplit::decode_split<1, false, kMixWaves>(m.de, e.y & ((1 << kHeadBits) - 1),
+                                                  e.y >> kHeadBits, e.x, lds.de);
+      } else {
+        const int2 e = tiles[j - dj];
+        atile::append_tile<kPosScale>(m.ap, e.y >> kHeadBits, e.y & ((1 << kHeadBits) - 1),
+                                      e.x, lds.ap);
+      }
     }
   }
 }
@@ -168,7 +241,7 @@ MixedLayout mixed_layout(int32_t B_decode, int32_t B_append, int32_t hq, int32_t
   l.qblocks = max_q_len > 0 ? (max_q_len + qpb - 1) / qpb : 0;
   l.max_tiles = (int64_t)B_append * l.qblocks * hkv_append;
   l.max_splits = (int64_t)B_decode * l.plan.max_splits * hkv_decode;
-  l.tiles_offset = kAlign;
+  l.tiles_offset = kAlign + align_up((size_t)(B_append > 0 ? B_append : 0) * sizeof(int32_t));
   l.splits_offset = l.tiles_offset + align_up((size_t)l.max_tiles * sizeof(int2));
   l.partials_offset = l.splits_offset + align_up((size_t)l.max_splits * sizeof(int2));
   l.bytes = l.partials_offset +
@@ -195,6 +268,7 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
                                   layout.plan.max_splits, layout.plan);
   m.header = reinterpret_cast<int32_t *>(ws);
   m.tiles = reinterpret_cast<int2 *>(ws + layout.tiles_offset);
+  m.order = reinterpret_cast<int32_t *>(ws + kAlign);
   m.splits = reinterpret_cast<int2 *>(ws + layout.splits_offset);
   m.B_append = B_append;
   m.qblocks = layout.qblocks;
