@@ -6,10 +6,13 @@ input at the Qwen3-8B GQA shape (Hq = 32, Hkv = 8, head dim 128, 16-token
 pages, bf16 K/V, fp32 outputs):
   1. kv_page_write  - the step's new tokens: one decode token per decode row
                       and every append row's observation chunk;
-  2. rollout_attn_decode - B = 64 trajectories, context uniform in
-                      [4096, 32768] keys, shuffled pages (split + combine kernels);
-  3. rollout_attn_append - B = 32 trajectories, cached context uniform in
-                      [2048, 24576], chunk uniform in [64, 2048] tokens.
+  2. rollout_attn_append - B = 32 trajectories, cached context uniform in
+                      [2048, 24576], chunk uniform in [64, 2048] tokens;
+  3. rollout_attn_decode - B = 64 trajectories, context uniform in
+                      [4096, 32768] keys, shuffled pages (split + combine kernels).
+Append runs before decode (the two are independent): the page write leaves
+its new tokens as dirty cache lines, and their write-back then overlaps the
+matrix-bound append instead of the HBM-bound decode.
 Inputs are resident in HBM before timing starts. Each call is bracketed by HIP
 events on the stream the library launches on (torch's current stream).
 
@@ -20,8 +23,8 @@ unmasked query-key pairs, two matrix products each) is reported beside it.
 `roofline` is the decode kernel pair against the 8 TB/s HBM peak,
 `roofline_append` the append kernel against the 2.5 PFLOP/s dense bf16 peak.
 `mixed_step` times the mixed rollout step on one pool (B = 512 trajectories,
-85 % decode rows / 15 % append rows, log-normal contexts: page write, decode,
-append on one stream) beside its lower bounds at the published peaks, and the
+85 % decode rows / 15 % append rows, log-normal contexts: page write, append,
+decode on one stream) beside its lower bounds at the published peaks, and the
 same step with decode and append rows in one persistent launch
 (`single_launch`).
 `shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
@@ -152,7 +155,7 @@ def cpu_baseline(wd, td, wa, ta, seconds: float):
 
 def mixed_step(ra, synth, dev, steps: int, warmup: int):
     """Time the mixed rollout step of one pool: page write of the step's new
-    tokens, decode of the decode rows, append of the append rows (85 % / 15 %
+    tokens, append of the append rows, decode of the decode rows (15 % / 85 %
     of B = 512 trajectories, log-normal contexts), on one stream."""
     import torch
 
@@ -185,11 +188,11 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
         ra.kv_page_write(t.k_new, t.v_new, cu_t, start_t, kv_w, max_new, max_pos)
         if ev is not None:
             ev[1].record()
-        ra.decode(t.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
-        if ev is not None:
-            ev[2].record()
         ra.append(t.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a,
                   workspace=ws_a)
+        if ev is not None:
+            ev[2].record()
+        ra.decode(t.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
         if ev is not None:
             ev[3].record()
 
@@ -225,8 +228,8 @@ def mixed_step(ra, synth, dev, steps: int, warmup: int):
     single_ms = np.mean([e[0].elapsed_time(e[2]) for e in ev_single])
     single_attn_ms = np.mean([e[1].elapsed_time(e[2]) for e in ev_single])
     w_ms = np.mean([e[0].elapsed_time(e[1]) for e in events])
-    d_ms = np.mean([e[1].elapsed_time(e[2]) for e in events])
-    a_ms = np.mean([e[2].elapsed_time(e[3]) for e in events])
+    a_ms = np.mean([e[1].elapsed_time(e[2]) for e in events])
+    d_ms = np.mean([e[2].elapsed_time(e[3]) for e in events])
     s_ms = np.mean([e[0].elapsed_time(e[3]) for e in events])
     dbytes, aflops = decode_bytes(w), append_flops(w)
     wbytes = write_bytes(int(cu[-1]), w.Hkv)
@@ -441,11 +444,11 @@ def main():
         ra.kv_page_write(ta.k_new, ta.v_new, cu_a_t, st_a_t, kv_aw, max_new_a, max_pos_a)
         if ev is not None:
             ev[1].record()
-        ra.decode(td.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
-        if ev is not None:
-            ev[2].record()
         ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv_a, SCALE, out=out_a,
                   workspace=ws_a)
+        if ev is not None:
+            ev[2].record()
+        ra.decode(td.q_decode, kv_d, kv_lens, max_kv_d, SCALE, out=out_d, workspace=ws)
         if ev is not None:
             ev[3].record()
 
@@ -480,8 +483,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     w_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
-    d_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
-    a_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+    a_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
+    d_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
     step_ms = np.array([e[0].elapsed_time(e[3]) for e in events])
 
     dbytes = decode_bytes(wd)
@@ -521,8 +524,8 @@ def main():
         "data": "synthetic (seeded; bf16 N(0,1) K/V/q, shuffled 16-token pages)",
         "config": {
             "workload": "rollout attention step, Qwen3-8B GQA (Hq=32, Hkv=8, d=128, page 16): "
-                        "page write + decode B=64 L~U[4096,32768] + append B=32 "
-                        "ctx~U[2048,24576] T~U[64,2048]",
+                        "page write + append B=32 ctx~U[2048,24576] T~U[64,2048] + "
+                        "decode B=64 L~U[4096,32768]",
             "decode_rows": int(wd.kv_lens.shape[0]),
             "decode_kv_tokens": int(wd.kv_lens.sum()),
             "append_rows": int(wa.q_lens.shape[0]),
