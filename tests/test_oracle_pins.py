@@ -423,3 +423,135 @@ def test_logprob_normalised_and_shift_invariant():
     shift = float(bits_f64(h)[0] @ w0)
     _, lse1 = oracle.token_logprob(np.repeat(h, V, 0), W, all_t)
     np.testing.assert_allclose(lse2, lse1 + shift, rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------- fp8 pools
+
+def test_e4m3_decode_matches_torch_for_every_code():
+    """The E4M3 value table against torch's float8_e4m3fn (a library routine)."""
+    c = np.arange(256, dtype=np.uint8)
+    mine = oracle.e4m3_decode(c)
+    ref = torch.from_numpy(c).view(torch.float8_e4m3fn).double().numpy()
+    assert np.array_equal(np.isnan(mine), np.isnan(ref))
+    assert np.isnan(mine[[0x7F, 0xFF]]).all() and np.isnan(mine).sum() == 2
+    ok = ~np.isnan(ref)
+    np.testing.assert_array_equal(mine[ok], ref[ok])
+    assert mine[0x7E] == 448.0 and mine[0x01] == 2.0 ** -9 and mine[0x38] == 1.0
+
+
+def test_e4m3_encode_matches_torch_in_range():
+    """Round to nearest (ties to even) against torch for every finite bf16 value within
+    +-448 and for random fp32 values across the subnormal and normal ranges."""
+    b = np.arange(1 << 16, dtype=np.uint32)
+    f = (b << 16).view(np.float32)
+    f = f[np.isfinite(f) & (np.abs(f) <= 448)]
+    rng = np.random.default_rng(3)
+    r = (rng.standard_normal(100000) * 2.0 ** rng.integers(-14, 9, 100000)).astype(np.float32)
+    x = np.concatenate([f, r[np.abs(r) <= 448]])
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    np.testing.assert_array_equal(oracle.e4m3_encode(x), ref)
+
+
+def test_e4m3_encode_closed_forms():
+    cases = [
+        (1.0, 0x38), (-1.0, 0xB8), (448.0, 0x7E), (-448.0, 0xFE),
+        (1.0625, 0x38),   # halfway between 1 and 1.125: the even code
+        (1.1875, 0x3A),   # halfway between 1.125 and 1.25: the even code
+        (2.0 ** -9, 0x01),   # smallest subnormal
+        (2.0 ** -10, 0x00),   # half of it: tie to the even code 0
+        (3 * 2.0 ** -10, 0x02),   # halfway between 2^-9 and 2^-8: even
+        (-0.0, 0x80), (0.0, 0x00),
+        (464.0, 0x7E), (1e6, 0x7E), (-1e6, 0xFE),   # saturation
+        (float("inf"), 0x7E), (float("-inf"), 0xFE),
+        (float("nan"), 0x7F),
+    ]
+    x = np.array([c[0] for c in cases], np.float64)
+    np.testing.assert_array_equal(oracle.e4m3_encode(x), np.array([c[1] for c in cases], np.uint8))
+    # decode(encode(v)) == v for every finite code's value
+    c = np.array([i for i in range(256) if i not in (0x7F, 0xFF)], np.uint8)
+    np.testing.assert_array_equal(oracle.e4m3_encode(oracle.e4m3_decode(c)), c)
+
+
+def _fp8_pools(rng, lens, Hkv, P, D):
+    """Paged fp8 pools holding random finite codes (the layout of place())."""
+    ks = [rng.integers(0, 0x7F, (Hkv, L, D)) | (rng.integers(0, 2, (Hkv, L, D)) << 7)
+          for L in lens]
+    vs = [rng.integers(0, 0x7F, (Hkv, L, D)) | (rng.integers(0, 2, (Hkv, L, D)) << 7)
+          for L in lens]
+    kp, vp, bt = place([k.astype(np.uint16) for k in ks], [v.astype(np.uint16) for v in vs], 0,
+                       Hkv, P, D, rng, fill=0)
+    return kp.astype(np.uint8), vp.astype(np.uint8), bt
+
+
+def test_fp8_page_write_quantizes_and_gathers_codes():
+    rng = np.random.default_rng(91)
+    Hkv, P, D = 2, 16, 128
+    old, new = [37, 0, 16, 5], [1, 20, 33, 0]
+    total = [o + n for o, n in zip(old, new)]
+    kp, vp, bt = _fp8_pools(rng, total, Hkv, P, D)
+    cu = np.concatenate([[0], np.cumsum(new)]).astype(np.int32)
+    k_new = randn_bits(rng, (int(cu[-1]), Hkv, D))
+    v_new = bf16_bits(rng.standard_normal((int(cu[-1]), Hkv, D)) * 300.0)   # some saturate
+    ks, vs = 0.05, 0.7
+    kp2, vp2 = oracle.page_write_fp8(k_new, v_new, cu, old, bt, kp, vp, ks, vs)
+    kq, vq = oracle.quantize(k_new, ks), oracle.quantize(v_new, vs)
+    kx, vx = kp.copy(), vp.copy()
+    for b in range(4):
+        for t in range(new[b]):
+            pos = old[b] + t
+            kx[bt[b, pos // P], :, pos % P, :] = kq[cu[b] + t]
+            vx[bt[b, pos // P], :, :, pos % P] = vq[cu[b] + t]
+    np.testing.assert_array_equal(kp2, kx)
+    np.testing.assert_array_equal(vp2, vx)
+    assert (vq == 0x7E).any() or (vq == 0xFE).any()
+    # the stored value is within half a quantum of x / scale (or saturated)
+    xk = bits_f64(k_new) / np.float32(ks)
+    dk = oracle.e4m3_decode(kq)
+    assert np.all(np.abs(dk - xk) <= np.maximum(np.abs(xk) * 2.0 ** -4, 2.0 ** -10) + 1e-12)
+    cu_out = np.concatenate([[0], np.cumsum(total)]).astype(np.int32)
+    ko, vo = oracle.page_gather_u8(kp2, vp2, bt, total, cu_out)
+    kd, vd = dense_rows(kp2, vp2, bt, total)
+    for b in range(4):
+        np.testing.assert_array_equal(ko[cu_out[b]:cu_out[b + 1]], kd[b].transpose(1, 0, 2))
+        np.testing.assert_array_equal(vo[cu_out[b]:cu_out[b + 1]], vd[b].transpose(1, 0, 2))
+
+
+@pytest.mark.parametrize("ks,vs", [(2.0 ** -3, 2.0 ** 2), (1.0, 2.0 ** -5)])
+def test_fp8_attention_equals_bf16_oracle_on_exact_values(ks, vs):
+    """With power-of-two scales every dequantized value is exactly a bf16 value, so
+    attention over the fp8 pools must equal the (pinned) bf16 oracle bitwise."""
+    rng = np.random.default_rng(int(ks * 64 + vs))
+    Hq, Hkv, P, D = 8, 2, 16, 128
+    lens = [1, 17, 40, 0, 33]
+    kp, vp, bt = _fp8_pools(rng, lens, Hkv, P, D)
+    kb = bf16_bits(oracle.e4m3_decode(kp) * ks)
+    vb = bf16_bits(oracle.e4m3_decode(vp) * vs)
+    np.testing.assert_array_equal(bits_f64(kb), oracle.e4m3_decode(kp) * ks)
+    q = randn_bits(rng, (len(lens), Hq, D))
+    a, la = oracle.decode_fp8(q, kp, vp, ks, vs, bt, lens, 0.03)
+    b, lb = oracle.decode(q, kb, vb, bt, lens, 0.03)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(la, lb)
+    T = [1, 5, 7, 0, 9]
+    T = [min(t, L) for t, L in zip(T, lens)]
+    ctx = [L - t for L, t in zip(lens, T)]
+    cu = np.concatenate([[0], np.cumsum(T)]).astype(np.int32)
+    qa = randn_bits(rng, (int(cu[-1]), Hq, D))
+    a, la = oracle.append_fp8(qa, cu, ctx, kp, vp, ks, vs, bt, 0.03)
+    b, lb = oracle.append(qa, cu, ctx, kb, vb, bt, 0.03)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(la, lb)
+
+
+def test_fp8_scale_laws():
+    """k_scale multiplies every score (it folds into the softmax scale); v_scale
+    multiplies the output and leaves lse unchanged."""
+    rng = np.random.default_rng(5)
+    Hq, Hkv, P, D = 4, 1, 16, 128
+    lens = [3, 50]
+    kp, vp, bt = _fp8_pools(rng, lens, Hkv, P, D)
+    q = randn_bits(rng, (2, Hq, D))
+    a, la = oracle.decode_fp8(q, kp, vp, 0.3, 1.7, bt, lens, 0.01)
+    b, lb = oracle.decode_fp8(q, kp, vp, 1.0, 1.0, bt, lens, 0.003)
+    np.testing.assert_allclose(a, 1.7 * b, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(la, lb, rtol=1e-12, atol=1e-12)
