@@ -27,6 +27,8 @@ unmasked query-key pairs, two matrix products each) is reported beside it.
 decode on one stream) beside its lower bounds at the published peaks, and the
 same step with decode and append rows in one persistent launch
 (`single_launch`).
+`fp8_kv_decode` times the decode workload over an fp8 (OCP E4M3) pool beside
+the bf16 pool (each alone).
 `shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
 rollouts whose rows share each task's prompt pages. `token_logprob` times the
 fused LM-head log-probability kernel at the Qwen3-8B head for 64 and 1024
@@ -335,6 +337,64 @@ def shared_prefix_leg(ra, synth, dev, steps: int, warmup: int):
     return res
 
 
+def fp8_decode_bytes(w) -> int:
+    """Algorithmic bytes of decode over fp8 pools: as decode_bytes with one byte per
+    K/V element."""
+    L = w.kv_lens.astype(np.int64)
+    D, P = w.head_dim, w.page_size
+    per_row = L * w.Hkv * D * 2 + w.Hq * D * 2 + w.Hq * D * 4 + 4 * ((L + P - 1) // P) + 4
+    return int(per_row.sum())
+
+
+def fp8_kv_leg(ra, synth, dev, wd, td, steps: int, warmup: int):
+    """Decode of the B = 64 decode workload over an fp8 (E4M3) pool beside the same
+    rows over the bf16 pool, each timed alone."""
+    import torch
+
+    def i32(x):
+        return torch.as_tensor(np.ascontiguousarray(np.asarray(x, np.int32)), device=dev)
+
+    ks = vs = 2.0 ** -5
+    gen = synth.value_generator(1234, dev)
+    n = wd.layout.num_pages
+    k8 = synth.randn_fp8_codes((n, wd.Hkv, 16, 128), gen, dev, ks)
+    v8 = synth.randn_fp8_codes((n, wd.Hkv, 128, 16), gen, dev, vs)
+    bt = i32(wd.decode_table())
+    kv8 = ra.PagedKV(k8, v8, bt, ks, vs)
+    kv16 = ra.PagedKV(td.k_pool, td.v_pool, bt)
+    lens, max_kv, B = i32(wd.kv_lens), int(wd.kv_lens.max()), wd.kv_lens.shape[0]
+    out = torch.empty((B, wd.Hq, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty(ra.decode_workspace_size(B, wd.Hq, wd.Hkv, max_kv), dtype=torch.uint8,
+                     device=dev)
+    ms = {}
+    for name, kv in (("bf16", kv16), ("fp8", kv8)):
+        def fn():
+            ra.decode(td.q_decode, kv, lens, max_kv, SCALE, out=out, workspace=ws)
+        for _ in range(warmup):
+            fn()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for e in ev:
+            e[0].record()
+            fn()
+            e[1].record()
+        torch.cuda.synchronize()
+        ms[name] = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    b16, b8 = decode_bytes(wd), fp8_decode_bytes(wd)
+    res = {
+        "workload": wd.name + ", fp8 E4M3 pool (per-pool scales)",
+        "steps": steps, "warmup": warmup,
+        "bf16_ms": round(ms["bf16"], 4), "fp8_ms": round(ms["fp8"], 4),
+        "speedup": round(ms["bf16"] / ms["fp8"], 3),
+        "fp8_algorithmic_bytes": b8,
+        "fp8_GB_s": round(b8 / (ms["fp8"] * 1e-3) / 1e9, 1),
+        "fp8_frac_hbm_peak": round(b8 / (ms["fp8"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "bf16_GB_s": round(b16 / (ms["bf16"] * 1e-3) / 1e9, 1),
+    }
+    del k8, v8, out, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def logprob_leg(ra, synth, dev, steps: int, warmup: int):
     """token_logprob on the Qwen3-8B LM head (V = 151936, D = 4096): a decode
     batch of 64 tokens (bound by reading W) and 1024 tokens (bound by the
@@ -383,6 +443,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-shared-prefix", action="store_true",
                     help="skip the shared-prefix decode leg (8 tasks x 8 rollouts)")
+    ap.add_argument("--no-fp8", action="store_true",
+                    help="skip the fp8 KV pool decode leg")
     ap.add_argument("--no-logprob", action="store_true",
                     help="skip the token log-probability leg (Qwen3-8B LM head)")
     ap.add_argument("--no-mixed", action="store_true",
@@ -497,6 +559,9 @@ def main():
     shared = None
     if not args.no_shared_prefix:
         shared = shared_prefix_leg(ra, synth, dev, args.steps, args.warmup)
+    fp8 = None
+    if not args.no_fp8:
+        fp8 = fp8_kv_leg(ra, synth, dev, wd, td, args.steps, args.warmup)
     logprob = None
     if not args.no_logprob:
         logprob = logprob_leg(ra, synth, dev, args.steps, args.warmup)
@@ -553,6 +618,7 @@ def main():
                             "traffic": measured_traffic("append")},
         "mixed_step": mixed,
         "shared_prefix_decode": shared,
+        "fp8_kv_decode": fp8,
         "token_logprob": logprob,
         "cpu_baseline": cpu_dec,
         "cpu_baseline_append": cpu_app,

@@ -40,15 +40,28 @@
  *   - Results are deterministic: the same inputs give bitwise the same
  *     outputs, independent of which physical pages the block table names.
  *
- * Paged KV layout (ABI version 1). Page size P = 16 tokens, head dim D = 128.
+ * Paged KV layout (ABI version 2). Page size P = 16 tokens, head dim D = 128.
  * Logical token j of row b lives in physical page bt[b * bt_stride + j / P]
- * at slot j % P. Within a page each KV head owns one contiguous 4 KiB block:
- *   K pool  bf16 [num_pages][Hkv][P][D]   element (page, g, slot, d) at
+ * at slot j % P. Within a page each KV head owns one contiguous block:
+ *   K pool  [num_pages][Hkv][P][D]   element (page, g, slot, d) at
  *           ((page * Hkv + g) * P + slot) * D + d           (token-major)
- *   V pool  bf16 [num_pages][Hkv][D][P]   element (page, g, slot, d) at
+ *   V pool  [num_pages][Hkv][D][P]   element (page, g, slot, d) at
  *           ((page * Hkv + g) * D + d) * P + slot           (dim-major)
  * V is stored dimension-major so that the matrix-core operand for P·V (keys
- * along the contraction dimension) is a contiguous 16-byte read.
+ * along the contraction dimension) is a contiguous read.
+ * Element types (kv_dtype):
+ *   RA_KV_BF16      bf16 (4 KiB per page and head);
+ *   RA_KV_FP8_E4M3  OCP FP8 E4M3 codes (2 KiB per page and head) with one
+ *                   scale per pool: an element's value is decode(code) *
+ *                   k_scale (K) or * v_scale (V). The paper is silent on KV
+ *                   precision; this halves the bytes decode streams. A bf16
+ *                   value x is stored as encode(fp32(x) * fp32(1 / scale)):
+ *                   round to nearest even, magnitudes beyond 448 (and
+ *                   infinities) saturate to +-448, NaN becomes 0x7F.
+ *   fp8 pools are supported by kv_page_write (quantizing), kv_page_gather
+ *   (codes copied out), rollout_attn_decode and
+ *   rollout_attn_decode_shared_prefix; the other entry points return
+ *   RA_ERR_UNSUPPORTED for them.
  */
 #ifndef ROLLOUT_ATTN_H
 #define ROLLOUT_ATTN_H
@@ -62,7 +75,7 @@
 extern "C" {
 #endif
 
-#define RA_ABI_VERSION 1
+#define RA_ABI_VERSION 2
 #define RA_PAGE_SIZE 16
 #define RA_HEAD_DIM 128
 
@@ -71,21 +84,27 @@ typedef enum {
   RA_ERR_NULL = 1,        /* a required pointer is NULL */
   RA_ERR_SHAPE = 2,       /* inconsistent sizes (negative, Hq % Hkv != 0, ...) */
   RA_ERR_UNSUPPORTED = 3, /* valid but not built: page_size != 16, head_dim != 128,
-                             decode group size Hq / Hkv > 16 */
+                             decode group size Hq / Hkv > 16, an unknown kv_dtype,
+                             an fp8 pool where it is not supported */
   RA_ERR_WORKSPACE = 4,   /* workspace smaller than the *_workspace_size value */
   RA_ERR_HIP = 5          /* a HIP launch failed (no device, bad stream, ...) */
 } ra_status;
 
+typedef enum { RA_KV_BF16 = 0, RA_KV_FP8_E4M3 = 1 } ra_kv_dtype;
+
 /* Caller-owned paged KV cache (device memory), see the layout above. */
 typedef struct {
-  void *k_pool;               /* bf16 [num_pages][num_kv_heads][page_size][head_dim] */
-  void *v_pool;               /* bf16 [num_pages][num_kv_heads][head_dim][page_size] */
+  void *k_pool;               /* [num_pages][num_kv_heads][page_size][head_dim] */
+  void *v_pool;               /* [num_pages][num_kv_heads][head_dim][page_size] */
   const int32_t *block_table; /* int32 [B][bt_stride]; row b of the call's batch */
   int32_t num_pages;
   int32_t bt_stride;          /* entries per block-table row (>= 1) */
   int32_t num_kv_heads;       /* Hkv */
   int32_t page_size;          /* must be 16 */
   int32_t head_dim;           /* must be 128 */
+  int32_t kv_dtype;           /* ra_kv_dtype of both pools */
+  float k_scale, v_scale;     /* fp8 pools: finite and > 0 (RA_ERR_SHAPE otherwise);
+                                 ignored for bf16 pools */
 } ra_paged_kv;
 
 /* ABI version of the loaded library (RA_ABI_VERSION). */
@@ -273,9 +292,11 @@ int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t 
 
 /*
  * Page write: scatter new tokens' keys and values into their pages, a bit
- * copy. Row b's new tokens are packed rows cu_new[b] .. cu_new[b+1]-1 of
- * k_new / v_new; token t of the row goes to logical position start_pos[b] + t.
- * No other pool byte changes. Rows of one call must not write the same slot.
+ * copy into bf16 pools, a quantization into fp8 pools (each element stored as
+ * encode(fp32(x) * fp32(1 / scale)), see the layout above). Row b's new
+ * tokens are packed rows cu_new[b] .. cu_new[b+1]-1 of k_new / v_new; token t
+ * of the row goes to logical position start_pos[b] + t. No other pool byte
+ * changes. Rows of one call must not write the same slot.
  *
  *   k_new, v_new  bf16 [total_new][Hkv][128] (token-major)
  *   cu_new        int32 [B+1]
@@ -291,11 +312,12 @@ int kv_page_write(const void *k_new, const void *v_new, const int32_t *cu_new,
 /*
  * Page gather (test and export helper): copy logical tokens 0 .. lens[b]-1 of
  * every row out of the pages into packed token-major arrays; row b starts at
- * packed row cu_out[b]. A bit copy.
+ * packed row cu_out[b]. A bit copy of the stored elements (E4M3 codes for fp8
+ * pools).
  *
  *   lens     int32 [B]; max_len host upper bound of lens (<= bt_stride * 16)
  *   cu_out   int32 [B+1]
- *   k_out, v_out  bf16 [total][Hkv][128]
+ *   k_out, v_out  [total][Hkv][128] of the pools' element type
  */
 int kv_page_gather(const ra_paged_kv *kv, const int32_t *lens, const int32_t *cu_out, int32_t B,
                    int32_t total, int32_t max_len, void *k_out, void *v_out,

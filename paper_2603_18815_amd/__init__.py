@@ -6,8 +6,9 @@ device pointers plus torch's current HIP stream to the library; every step of
 the computation runs in the library's HIP kernels. If the library is not built
 the import of any function fails loudly: there is no fallback path.
 
-Layout (see the header): K pool bf16 [pages][Hkv][16][128] (token-major),
-V pool bf16 [pages][Hkv][128][16] (dim-major), block table int32 [B][stride].
+Layout (see the header): K pool [pages][Hkv][16][128] (token-major), V pool
+[pages][Hkv][128][16] (dim-major), block table int32 [B][stride]. Pools are
+bf16, or uint8 OCP FP8 E4M3 codes with one scale per pool (value = code * scale).
 """
 from __future__ import annotations
 
@@ -59,12 +60,27 @@ def _stream(device: torch.device, stream) -> int:
 
 
 class PagedKV:
-    """A caller-owned paged KV cache: two pools and a block table, all on one GPU."""
+    """A caller-owned paged KV cache: two pools and a block table, all on one GPU.
 
-    def __init__(self, k_pool: torch.Tensor, v_pool: torch.Tensor, block_table: torch.Tensor):
+    bf16 pools, or fp8 pools (torch.uint8 or torch.float8_e4m3fn storage of E4M3
+    codes) with k_scale / v_scale: an element's value is code * scale.
+    """
+
+    def __init__(self, k_pool: torch.Tensor, v_pool: torch.Tensor, block_table: torch.Tensor,
+                 k_scale: Optional[float] = None, v_scale: Optional[float] = None):
         dev = k_pool.device
-        _need(k_pool, "k_pool", torch.bfloat16, dev)
-        _need(v_pool, "v_pool", torch.bfloat16, dev)
+        if k_pool.dtype == torch.float8_e4m3fn:
+            k_pool = k_pool.view(torch.uint8)
+        if v_pool.dtype == torch.float8_e4m3fn:
+            v_pool = v_pool.view(torch.uint8)
+        self.fp8 = k_pool.dtype == torch.uint8
+        dt = torch.uint8 if self.fp8 else torch.bfloat16
+        _need(k_pool, "k_pool", dt, dev)
+        _need(v_pool, "v_pool", dt, dev)
+        if self.fp8 and (k_scale is None or v_scale is None):
+            raise ValueError("fp8 pools need k_scale and v_scale")
+        self.k_scale = float(k_scale) if self.fp8 else 1.0
+        self.v_scale = float(v_scale) if self.fp8 else 1.0
         _need(block_table, "block_table", torch.int32, dev)
         if k_pool.dim() != 4 or k_pool.shape[2:] != (PAGE_SIZE, HEAD_DIM):
             raise ValueError(f"k_pool must be [pages][Hkv][16][128], got {tuple(k_pool.shape)}")
@@ -80,12 +96,15 @@ class PagedKV:
 
     def with_table(self, block_table: torch.Tensor) -> "PagedKV":
         """Same pools, another block table (e.g. a sub-batch of rows)."""
-        return PagedKV(self.k_pool, self.v_pool, block_table)
+        return PagedKV(self.k_pool, self.v_pool, block_table,
+                       self.k_scale if self.fp8 else None, self.v_scale if self.fp8 else None)
 
     def struct(self) -> _lib.RaPagedKV:
         return _lib.RaPagedKV(self.k_pool.data_ptr(), self.v_pool.data_ptr(),
                               self.block_table.data_ptr(), self.num_pages, self.bt_stride,
-                              self.num_kv_heads, PAGE_SIZE, HEAD_DIM)
+                              self.num_kv_heads, PAGE_SIZE, HEAD_DIM,
+                              _lib.RA_KV_FP8_E4M3 if self.fp8 else _lib.RA_KV_BF16,
+                              self.k_scale, self.v_scale)
 
 
 def abi_version() -> int:
@@ -319,7 +338,8 @@ def mixed(q_decode: torch.Tensor, kv_decode: PagedKV, kv_lens: torch.Tensor,
 def kv_page_write(k_new: torch.Tensor, v_new: torch.Tensor, cu_new: torch.Tensor,
                   start_pos: torch.Tensor, kv: PagedKV, max_new: Optional[int] = None,
                   max_pos: Optional[int] = None, stream=None) -> None:
-    """Scatter packed new tokens (bf16 [N][Hkv][128]) into the pages (bit copy)."""
+    """Scatter packed new tokens (bf16 [N][Hkv][128]) into the pages (a bit copy into
+    bf16 pools, quantized to E4M3 codes in fp8 pools)."""
     lib = _lib.load()
     dev = kv.device
     _need(k_new, "k_new", torch.bfloat16, dev)
@@ -346,7 +366,8 @@ def kv_page_write(k_new: torch.Tensor, v_new: torch.Tensor, cu_new: torch.Tensor
 def kv_page_gather(kv: PagedKV, lens: torch.Tensor, cu_out: torch.Tensor,
                    total: Optional[int] = None, max_len: Optional[int] = None, stream=None
                    ) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Copy logical tokens [0, lens[b]) of every row out to packed bf16 [total][Hkv][128]."""
+    """Copy logical tokens [0, lens[b]) of every row out to packed [total][Hkv][128]
+    (bf16, or uint8 E4M3 codes for fp8 pools)."""
     lib = _lib.load()
     dev = kv.device
     _need(lens, "lens", torch.int32, dev)
@@ -358,7 +379,8 @@ def kv_page_gather(kv: PagedKV, lens: torch.Tensor, cu_out: torch.Tensor,
         total = int(cu_out[-1].item()) if B else 0
     if max_len is None:
         max_len = int(lens.max().item()) if B else 0
-    k_out = torch.empty((total, kv.num_kv_heads, HEAD_DIM), dtype=torch.bfloat16, device=dev)
+    k_out = torch.empty((total, kv.num_kv_heads, HEAD_DIM),
+                        dtype=torch.uint8 if kv.fp8 else torch.bfloat16, device=dev)
     v_out = torch.empty_like(k_out)
     s = kv.struct()
     _lib.check("kv_page_gather", lib.kv_page_gather(

@@ -12,6 +12,9 @@ RA_ERR_UNSUPPORTED = 3
 RA_ERR_WORKSPACE = 4
 RA_ERR_HIP = 5
 
+RA_KV_BF16 = 0
+RA_KV_FP8_E4M3 = 1
+
 EXPORTS = (
     "ra_abi_version",
     "ra_status_string",
@@ -40,6 +43,9 @@ class RaPagedKV(ctypes.Structure):
         ("num_kv_heads", ctypes.c_int32),
         ("page_size", ctypes.c_int32),
         ("head_dim", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+        ("k_scale", ctypes.c_float),
+        ("v_scale", ctypes.c_float),
     ]
 
 

@@ -2,6 +2,8 @@
 // call), launch planning and status codes. See include/rollout_attn.h.
 #include "rollout_attn.h"
 
+#include <cmath>
+
 #include "ra_internal.h"
 
 namespace {
@@ -16,9 +18,16 @@ int check_kv(const ra_paged_kv *kv) {
   if (kv->page_size != RA_PAGE_SIZE || kv->head_dim != RA_HEAD_DIM) return RA_ERR_UNSUPPORTED;
   if (kv->num_kv_heads <= 0 || kv->num_pages <= 0 || kv->bt_stride <= 0) return RA_ERR_SHAPE;
   if (kv->num_kv_heads > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (kv->kv_dtype != RA_KV_BF16 && kv->kv_dtype != RA_KV_FP8_E4M3) return RA_ERR_UNSUPPORTED;
+  if (kv->kv_dtype == RA_KV_FP8_E4M3 &&
+      !(std::isfinite(kv->k_scale) && kv->k_scale > 0.f && std::isfinite(kv->v_scale) &&
+        kv->v_scale > 0.f))
+    return RA_ERR_SHAPE;
   if (!kv->k_pool || !kv->v_pool || !kv->block_table) return RA_ERR_NULL;
   return RA_OK;
 }
+
+bool is_fp8(const ra_paged_kv *kv) { return kv->kv_dtype == RA_KV_FP8_E4M3; }
 
 bool positions_fit(const ra_paged_kv *kv, int32_t max_pos) {
   return max_pos >= 0 && (int64_t)max_pos <= (int64_t)kv->bt_stride * RA_PAGE_SIZE;
@@ -32,6 +41,9 @@ ra::PagedKV to_internal(const ra_paged_kv *kv) {
   p.num_pages = kv->num_pages;
   p.bt_stride = kv->bt_stride;
   p.hkv = kv->num_kv_heads;
+  p.fp8 = is_fp8(kv);
+  p.k_scale = p.fp8 ? kv->k_scale : 1.f;
+  p.v_scale = p.fp8 ? kv->v_scale : 1.f;
   return p;
 }
 
@@ -130,6 +142,7 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
   int s = check_kv(kv);
   if (s != RA_OK) return s;
   if (!q || !cu_q || !ctx_lens || !out) return RA_ERR_NULL;
+  if (is_fp8(kv)) return RA_ERR_UNSUPPORTED;
   if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
   if (Hq / kv->num_kv_heads > 256 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
   if (!positions_fit(kv, max_kv_len) || max_q_len > max_kv_len) return RA_ERR_SHAPE;
@@ -178,6 +191,7 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
   if (dec) {
     if ((s = check_kv(kv_decode)) != RA_OK) return s;
     if (!q_decode || !kv_lens || !out_decode) return RA_ERR_NULL;
+    if (is_fp8(kv_decode)) return RA_ERR_UNSUPPORTED;
     if (Hq % kv_decode->num_kv_heads != 0) return RA_ERR_SHAPE;
     if (Hq / kv_decode->num_kv_heads > 16 || B_decode > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
     if (!positions_fit(kv_decode, max_kv_len_decode)) return RA_ERR_SHAPE;
@@ -185,6 +199,7 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
   if (app) {
     if ((s = check_kv(kv_append)) != RA_OK) return s;
     if (!q_append || !cu_q || !ctx_lens || !out_append) return RA_ERR_NULL;
+    if (is_fp8(kv_append)) return RA_ERR_UNSUPPORTED;
     if (Hq % kv_append->num_kv_heads != 0) return RA_ERR_SHAPE;
     if (Hq / kv_append->num_kv_heads > 256) return RA_ERR_UNSUPPORTED;
     if (!positions_fit(kv_append, max_kv_len_append) || max_q_len > max_kv_len_append)

@@ -15,10 +15,20 @@ constexpr int kSplitWaves = 4;
 // KV head fastest: the Hkv workgroups of one (item, split) are dispatched
 // together, so the Hkv adjacent 4 KiB blocks of every page they read are
 // requested close in time (DRAM row locality).
-template <int NT, bool kPrefix>
+template <int NT, bool kPrefix, bool kFp8>
 __global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_kernel(DecodeArgs a) {
   __shared__ DecodeLds<NT, kSplitWaves> lds;
-  decode_split<NT, kPrefix, kSplitWaves>(a, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+  decode_split<NT, kPrefix, kSplitWaves, kFp8>(a, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+}
+
+template <int NT, bool kPrefix>
+void launch_split(bool fp8, dim3 grid, const DecodeArgs &a, hipStream_t stream) {
+  if (fp8)
+    hipLaunchKernelGGL((decode_split_kernel<NT, kPrefix, true>), grid, dim3(kSplitWaves * kWave),
+                       0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_split_kernel<NT, kPrefix, false>), grid, dim3(kSplitWaves * kWave),
+                       0, stream, a);
 }
 
 }  // namespace
@@ -64,8 +74,7 @@ hipError_t launch_decode(const uint16_t *q, const PagedKV &kv, const int32_t *kv
                          void *workspace, const DecodePlan &plan, hipStream_t stream) {
   const DecodeArgs a =
       make_decode_args(q, kv, kv_lens, B, hq, max_kv_len, scale, workspace, plan.max_splits, plan);
-  hipLaunchKernelGGL((decode_split_kernel<1, false>), dim3(kv.hkv, plan.max_splits, B),
-                     dim3(kSplitWaves * kWave), 0, stream, a);
+  launch_split<1, false>(kv.fp8, dim3(kv.hkv, plan.max_splits, B), a, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(hq, B), dim3(kHeadDim), 0, stream, a, out, lse);
@@ -102,14 +111,13 @@ hipError_t launch_decode_shared_prefix(const uint16_t *q, const PagedKV &kv,
     a.zdiv = sh.chunks;
     const dim3 grid(kv.hkv, ps, (unsigned)sh.prefix_z);
     if (sh.tiles == 1)
-      hipLaunchKernelGGL((decode_split_kernel<1, true>), grid, dim3(kSplitWaves * kWave), 0, stream, a);
+      launch_split<1, true>(kv.fp8, grid, a, stream);
     else
-      hipLaunchKernelGGL((decode_split_kernel<2, true>), grid, dim3(kSplitWaves * kWave), 0, stream, a);
+      launch_split<2, true>(kv.fp8, grid, a, stream);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   a.zdiv = max_group_rows;
-  hipLaunchKernelGGL((decode_split_kernel<1, false>), dim3(kv.hkv, plan.max_splits, (unsigned)sh.row_z),
-                     dim3(kSplitWaves * kWave), 0, stream, a);
+  launch_split<1, false>(kv.fp8, dim3(kv.hkv, plan.max_splits, (unsigned)sh.row_z), a, stream);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(hq, (unsigned)sh.row_z), dim3(kHeadDim), 0, stream,
                      a, out, lse);

@@ -55,7 +55,8 @@ struct DecodeArgs {
   int32_t prefix_slots;   // slots [0, prefix_slots) hold prefix splits (0: plain decode)
   int32_t zdiv;           // shared prefix: work items per group along grid z
   int32_t rows_per_chunk; // shared prefix: rows of a group one prefix workgroup covers
-  float scale_log2;
+  float scale_log2;       // softmax scale * log2(e) (* k_scale for fp8 pools)
+  float v_scale;          // multiplies the output (1 for bf16 pools)
 };
 
 __device__ __forceinline__ int row_len(const DecodeArgs &a, int b) {
@@ -91,8 +92,9 @@ struct DecodeLds {
 };
 
 // One split of KV head g (work item z: a row, or a group's row chunk), by a
-// workgroup of kW waves that all call it with the same arguments.
-template <int NT, bool kPrefix, int kW>
+// workgroup of kW waves that all call it with the same arguments. kFp8: the
+// pools hold E4M3 codes, converted exactly to bf16 operands after the load.
+template <int NT, bool kPrefix, int kW, bool kFp8 = false>
 __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int split, int z,
                                              DecodeLds<NT, kW> &lds) {
   // ---- what this workgroup computes: keys [t0, t1) of row krow's table for
@@ -136,16 +138,20 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
   const int G = a.group;
 
   // Q^T operands: column 16 nt + col = (row r0 + c / G, head c % G), dims
-  // 32 kk + 8 kgrp + 0..7.
+  // 32 kk + 8 kgrp + 0..7 (bf16 pools), or 64 (kk / 2) + 16 kgrp + 8 (kk % 2)
+  // + 0..7 (fp8 pools: a lane then reads 16 contiguous K bytes per 64 dims).
+  // Any order of the contraction is valid as long as K follows the same one.
   bf16x8 qop[NT][4];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int c = 16 * nt + col, r = c / G;
     if (r < nr) {
-      const uint16_t *qp =
-          a.q + ((size_t)(r0 + r) * a.hq + (size_t)g * G + (c - r * G)) * kHeadDim + 8 * kgrp;
+      const uint16_t *qrow =
+          a.q + ((size_t)(r0 + r) * a.hq + (size_t)g * G + (c - r * G)) * kHeadDim;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = load_bf16x8(qp + 32 * kk);
+      for (int kk = 0; kk < 4; ++kk)
+        qop[nt][kk] = kFp8 ? load_bf16x8(qrow + 64 * (kk >> 1) + 16 * kgrp + 8 * (kk & 1))
+                           : load_bf16x8(qrow + 32 * kk + 8 * kgrp);
     } else {
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = bf16x8{};
@@ -179,19 +185,41 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
     const int id0 = clamp_page(bt[pg], a.num_pages);
     const int id1 = pg + 1 < row_pages ? clamp_page(bt[pg + 1], a.num_pages) : id0;
 
-    const uint16_t *kb =
-        a.k_pool + ((size_t)(ka_sel ? id1 : id0) * a.hkv + g) * head_stride;
     bf16x8 ka[2][4];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        ka[t][kk] = load_bf16x8(kb + (ka_slot + 4 * t) * kHeadDim + 32 * kk + 8 * kgrp);
-    const uint16_t *vb =
-        a.v_pool + ((size_t)(sv_sel ? id1 : id0) * a.hkv + g) * head_stride;
     bf16x8 va[8];
+    if constexpr (kFp8) {
+      // one byte per element: K rows as 2 x 16 bytes per lane, V as 8 bytes
+      const uint8_t *kb = reinterpret_cast<const uint8_t *>(a.k_pool) +
+                          ((size_t)(ka_sel ? id1 : id0) * a.hkv + g) * head_stride;
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) va[mt] = load_bf16x8(vb + (16 * mt + col) * kPage + sv_slot);
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const u32x4 w = *reinterpret_cast<const u32x4 *>(kb + (ka_slot + 4 * t) * kHeadDim +
+                                                             64 * h + 16 * kgrp);
+          ka[t][2 * h] = fp8x8_to_bf16x8(u32x2{w[0], w[1]});
+          ka[t][2 * h + 1] = fp8x8_to_bf16x8(u32x2{w[2], w[3]});
+        }
+      const uint8_t *vb = reinterpret_cast<const uint8_t *>(a.v_pool) +
+                          ((size_t)(sv_sel ? id1 : id0) * a.hkv + g) * head_stride;
+#pragma unroll
+      for (int mt = 0; mt < 8; ++mt)
+        va[mt] = fp8x8_to_bf16x8(
+            *reinterpret_cast<const u32x2 *>(vb + (16 * mt + col) * kPage + sv_slot));
+    } else {
+      const uint16_t *kb =
+          a.k_pool + ((size_t)(ka_sel ? id1 : id0) * a.hkv + g) * head_stride;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          ka[t][kk] = load_bf16x8(kb + (ka_slot + 4 * t) * kHeadDim + 32 * kk + 8 * kgrp);
+      const uint16_t *vb =
+          a.v_pool + ((size_t)(sv_sel ? id1 : id0) * a.hkv + g) * head_stride;
+#pragma unroll
+      for (int mt = 0; mt < 8; ++mt)
+        va[mt] = load_bf16x8(vb + (16 * mt + col) * kPage + sv_slot);
+    }
 
     // Keys at or past t1 are not attended: their scores become -inf and
     // their V entries are replaced (not multiplied) by zero, so that
@@ -335,7 +363,7 @@ __global__ __launch_bounds__(kHeadDim) void decode_combine_kernel(DecodeArgs a, 
     acc += f * o[(size_t)k * kHeadDim];
     lsum += f * l[k];
   }
-  out[bh * kHeadDim + d] = acc / lsum;
+  out[bh * kHeadDim + d] = acc / lsum * a.v_scale;
   if (lse && d == 0) lse[bh] = (M + __log2f(lsum)) * kLn2;
 }
 
@@ -368,7 +396,8 @@ inline DecodeArgs make_decode_args(const uint16_t *q, const PagedKV &kv, const i
   a.prefix_slots = 0;
   a.zdiv = 1;
   a.rows_per_chunk = 1;
-  a.scale_log2 = scale * kLog2e;
+  a.scale_log2 = scale * kLog2e * kv.k_scale;
+  a.v_scale = kv.v_scale;
   return a;
 }
 

@@ -61,6 +61,46 @@ __device__ __forceinline__ float col_sum4(float x) {
   return x;
 }
 
+// ---- fp8 pools: OCP E4M3 codes ----
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Eight E4M3 codes (byte i of the pair of words = element i) -> bf16, exact:
+// every E4M3 value is a bf16 value.
+__device__ __forceinline__ bf16x8 fp8x8_to_bf16x8(u32x2 w) {
+  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, false);
+  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, true);
+  const bf16x2 c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, false);
+  const bf16x2 d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, true);
+  return bf16x8{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
+}
+
+// E4M3 codes of two fp32 values in the low 16 bits (element 0 in byte 0):
+// round to nearest even, saturated to +-448 (infinities included), NaN ->
+// 0x7F.
+__device__ __forceinline__ uint32_t fp8_pair(float x, float y) {
+  const float cx = fminf(fmaxf(x, -448.f), 448.f), cy = fminf(fmaxf(y, -448.f), 448.f);
+  uint32_t w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(cx, cy, 0, false) & 0xffffu;
+  w = x != x ? ((w & 0xff00u) | 0x7fu) : w;
+  w = y != y ? ((w & 0x00ffu) | 0x7f00u) : w;
+  return w;
+}
+
+// Eight bf16 values (16 bytes) -> eight E4M3 codes of x * inv_scale (the
+// product rounded to fp32).
+__device__ __forceinline__ u32x2 quantize8(u32x4 v, float inv_scale) {
+  u32x2 r;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t lo = fp8_pair(__uint_as_float(v[2 * h] << 16) * inv_scale,
+                                 __uint_as_float(v[2 * h] & 0xffff0000u) * inv_scale);
+    const uint32_t hi = fp8_pair(__uint_as_float(v[2 * h + 1] << 16) * inv_scale,
+                                 __uint_as_float(v[2 * h + 1] & 0xffff0000u) * inv_scale);
+    r[h] = lo | (hi << 16);
+  }
+  return r;
+}
+
 __device__ __forceinline__ int clamp_page(int id, int num_pages) {
   return min(max(id, 0), num_pages - 1);
 }

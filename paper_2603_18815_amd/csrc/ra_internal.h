@@ -9,6 +9,8 @@
 
 namespace ra {
 
+// Pools hold bf16 elements, or E4M3 codes (fp8) whose value is code * scale;
+// k_pool / v_pool then point at bytes.
 struct PagedKV {
   uint16_t *k_pool;
   uint16_t *v_pool;
@@ -16,6 +18,8 @@ struct PagedKV {
   int32_t num_pages;
   int32_t bt_stride;
   int32_t hkv;
+  bool fp8;
+  float k_scale, v_scale;   // fp8 pools only (1 for bf16)
 };
 
 // ---- decode (split over pages, then combine) ----

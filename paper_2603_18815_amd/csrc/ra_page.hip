@@ -1,7 +1,10 @@
-// Page write and page gather: bit copies between packed token-major K/V rows
-// and the paged pools (K pages token-major [16][128], V pages dim-major
-// [128][16]). One workgroup moves one (row, page, KV head) block of 4 KiB per
-// pool; V goes through LDS so that both sides are accessed 16 bytes per lane.
+// Page write and page gather between packed token-major K/V rows and the
+// paged pools (K pages token-major [16][128], V pages dim-major [128][16]).
+// One workgroup moves one (row, page, KV head) block per pool; V goes through
+// LDS so that both sides are accessed in 8- or 16-byte pieces per lane.
+// bf16 pools: bit copies. fp8 pools: the write quantizes each bf16 element to
+// its E4M3 code (x * fp32(1 / scale), round to nearest even, saturated), the
+// gather copies the codes out.
 #include "ra_device.h"
 #include "ra_internal.h"
 
@@ -93,6 +96,84 @@ __global__ __launch_bounds__(kThreads) void page_gather_kernel(
   }
 }
 
+// fp8 pools: one byte per element; a lane quantizes 8 elements (16 bytes of
+// bf16 in, 8 bytes of codes out).
+__global__ __launch_bounds__(kThreads) void page_write_fp8_kernel(
+    const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
+    const int32_t *__restrict__ cu_new, const int32_t *__restrict__ start_pos,
+    uint8_t *__restrict__ k_pool, uint8_t *__restrict__ v_pool,
+    const int32_t *__restrict__ block_table, int bt_stride, int num_pages, int hkv,
+    int total_new, int max_new, int max_pos, float k_inv, float v_inv) {
+  const int chunk = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int cu0 = min(max(cu_new[b], 0), total_new);
+  const int n = min(min(max(cu_new[b + 1] - cu0, 0), max_new), total_new - cu0);
+  if (n <= 0) return;
+  const int s = min(max(start_pos[b], 0), max_pos - n);
+  if (s < 0) return;
+  const int pg = s / kPage + chunk;
+  if (pg > (s + n - 1) / kPage) return;
+  const int lo = max(s, pg * kPage), hi = min(s + n, pg * kPage + kPage);
+  const int id = clamp_page(block_table[(size_t)b * bt_stride + pg], num_pages);
+
+  __shared__ uint16_t sv[kPage][kVPitch];
+  const int slot = tid >> 4, ch = tid & 15;
+  const int pos = pg * kPage + slot;
+  if (pos >= lo && pos < hi) {
+    const size_t src = ((size_t)(cu0 + pos - s) * hkv + g) * kHeadDim + ch * 8;
+    const size_t dst = (((size_t)id * hkv + g) * kPage + slot) * kHeadDim + ch * 8;
+    *reinterpret_cast<u32x2 *>(k_pool + dst) = quantize8(load_u32x4(k_new + src), k_inv);
+    *reinterpret_cast<u32x4 *>(&sv[slot][ch * 8]) = load_u32x4(v_new + src);
+  }
+  __syncthreads();
+  const int d = tid >> 1, s0 = (tid & 1) * 8;
+  uint8_t *dst = v_pool + (((size_t)id * hkv + g) * kHeadDim + d) * kPage + s0;
+  const int p0 = pg * kPage + s0;
+  u32x4 t;
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    t[e] = (uint32_t)sv[s0 + 2 * e][d] | ((uint32_t)sv[s0 + 2 * e + 1][d] << 16);
+  const u32x2 q = quantize8(t, v_inv);
+  if (p0 >= lo && p0 + 8 <= hi) {
+    *reinterpret_cast<u32x2 *>(dst) = q;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (p0 + e >= lo && p0 + e < hi) dst[e] = (uint8_t)(q[e >> 2] >> (8 * (e & 3)));
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void page_gather_fp8_kernel(
+    const uint8_t *__restrict__ k_pool, const uint8_t *__restrict__ v_pool,
+    const int32_t *__restrict__ block_table, int bt_stride, int num_pages, int hkv,
+    const int32_t *__restrict__ lens, const int32_t *__restrict__ cu_out, int total, int max_len,
+    uint8_t *__restrict__ k_out, uint8_t *__restrict__ v_out) {
+  const int pg = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int cu0 = min(max(cu_out[b], 0), total);
+  const int L = min(min(max(lens[b], 0), max_len), total - cu0);
+  if (pg * kPage >= L) return;
+  const int id = clamp_page(block_table[(size_t)b * bt_stride + pg], num_pages);
+
+  __shared__ uint8_t sv[kPage][kHeadDim + 16];
+  {
+    const int d = tid >> 1, s0 = (tid & 1) * 8;
+    const u32x2 w = *reinterpret_cast<const u32x2 *>(
+        v_pool + (((size_t)id * hkv + g) * kHeadDim + d) * kPage + s0);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sv[s0 + e][d] = (uint8_t)(w[e >> 2] >> (8 * (e & 3)));
+  }
+  __syncthreads();
+  const int slot = tid >> 4, ch = tid & 15;
+  const int pos = pg * kPage + slot;
+  if (pos < L) {
+    const size_t dst = ((size_t)(cu0 + pos) * hkv + g) * kHeadDim + ch * 8;
+    const size_t src = (((size_t)id * hkv + g) * kPage + slot) * kHeadDim + ch * 8;
+    *reinterpret_cast<u32x2 *>(k_out + dst) = *reinterpret_cast<const u32x2 *>(k_pool + src);
+    *reinterpret_cast<u32x2 *>(v_out + dst) = *reinterpret_cast<const u32x2 *>(&sv[slot][ch * 8]);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
@@ -101,9 +182,16 @@ hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const
                              hipStream_t stream) {
   // A run of n tokens touches at most (n - 1) / 16 + 2 pages.
   const dim3 grid((max_new + kPage - 1) / kPage + 1, kv.hkv, B);
-  hipLaunchKernelGGL(page_write_kernel, grid, dim3(kThreads), 0, stream, k_new, v_new, cu_new,
-                     start_pos, kv.k_pool, kv.v_pool, kv.block_table, kv.bt_stride, kv.num_pages,
-                     kv.hkv, total_new, max_new, max_pos);
+  if (kv.fp8)
+    hipLaunchKernelGGL(page_write_fp8_kernel, grid, dim3(kThreads), 0, stream, k_new, v_new,
+                       cu_new, start_pos, reinterpret_cast<uint8_t *>(kv.k_pool),
+                       reinterpret_cast<uint8_t *>(kv.v_pool), kv.block_table, kv.bt_stride,
+                       kv.num_pages, kv.hkv, total_new, max_new, max_pos, 1.0f / kv.k_scale,
+                       1.0f / kv.v_scale);
+  else
+    hipLaunchKernelGGL(page_write_kernel, grid, dim3(kThreads), 0, stream, k_new, v_new, cu_new,
+                       start_pos, kv.k_pool, kv.v_pool, kv.block_table, kv.bt_stride,
+                       kv.num_pages, kv.hkv, total_new, max_new, max_pos);
   return hipGetLastError();
 }
 
@@ -111,9 +199,16 @@ hipError_t launch_page_gather(const PagedKV &kv, const int32_t *lens, const int3
                               int32_t B, int32_t total, int32_t max_len, uint16_t *k_out,
                               uint16_t *v_out, hipStream_t stream) {
   const dim3 grid((max_len + kPage - 1) / kPage, kv.hkv, B);
-  hipLaunchKernelGGL(page_gather_kernel, grid, dim3(kThreads), 0, stream, kv.k_pool, kv.v_pool,
-                     kv.block_table, kv.bt_stride, kv.num_pages, kv.hkv, lens, cu_out, total,
-                     max_len, k_out, v_out);
+  if (kv.fp8)
+    hipLaunchKernelGGL(page_gather_fp8_kernel, grid, dim3(kThreads), 0, stream,
+                       reinterpret_cast<const uint8_t *>(kv.k_pool),
+                       reinterpret_cast<const uint8_t *>(kv.v_pool), kv.block_table, kv.bt_stride,
+                       kv.num_pages, kv.hkv, lens, cu_out, total, max_len,
+                       reinterpret_cast<uint8_t *>(k_out), reinterpret_cast<uint8_t *>(v_out));
+  else
+    hipLaunchKernelGGL(page_gather_kernel, grid, dim3(kThreads), 0, stream, kv.k_pool, kv.v_pool,
+                       kv.block_table, kv.bt_stride, kv.num_pages, kv.hkv, lens, cu_out, total,
+                       max_len, k_out, v_out);
   return hipGetLastError();
 }
 

@@ -262,6 +262,20 @@ def randn_bf16(shape, gen: torch.Generator, device, chunk: int = 1 << 28) -> tor
     return out
 
 
+def randn_fp8_codes(shape, gen: torch.Generator, device, scale: float,
+                    chunk: int = 1 << 28) -> torch.Tensor:
+    """E4M3 codes (uint8) of N(0,1) values stored with the given pool scale: N(0,1) / scale
+    clamped to +-448 and rounded to E4M3 by torch (round to nearest even)."""
+    out = torch.empty(shape, dtype=torch.uint8, device=device)
+    flat = out.view(-1)
+    n = flat.numel()
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        x = torch.randn(e - s, generator=gen, device=device, dtype=torch.float32) / scale
+        flat[s:e] = x.clamp(-448.0, 448.0).to(torch.float8_e4m3fn).view(torch.uint8)
+    return out
+
+
 @dataclasses.dataclass
 class Tensors:
     k_pool: torch.Tensor     # bf16 [pages][Hkv][16][128]
@@ -304,13 +318,16 @@ def write_plan(w: Workload):
 
 def poison_unowned(k_pool: torch.Tensor, v_pool: torch.Tensor, layout: PagedLayout,
                    rows=None, lens=None) -> None:
-    """Fill decoy pages and every slot past each row's length with bf16 NaN (in place).
+    """Fill decoy pages and every slot past each row's length with NaN (in place).
 
     rows/lens: the rows whose tail slots to poison and their lengths in tokens
     (defaults: every row, its resident token count).
     """
     P = k_pool.shape[2]
-    nan = torch.tensor(BF16_NAN, dtype=torch.int16).view(torch.bfloat16).item()
+    if k_pool.dtype == torch.uint8:      # fp8 pools: the E4M3 NaN code
+        nan = 0x7F
+    else:
+        nan = torch.tensor(BF16_NAN, dtype=torch.int16).view(torch.bfloat16).item()
     dec = torch.as_tensor(layout.decoys.astype(np.int64), device=k_pool.device)
     k_pool[dec] = nan
     v_pool[dec] = nan
@@ -328,8 +345,12 @@ def poison_unowned(k_pool: torch.Tensor, v_pool: torch.Tensor, layout: PagedLayo
 # ---------------------------------------------------------------------------
 
 def bits(t: torch.Tensor) -> np.ndarray:
-    """bf16 tensor (any device) -> host uint16 bit patterns."""
-    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    """bf16 tensor (any device) -> host uint16 bit patterns; a uint8 tensor (E4M3
+    codes of an fp8 pool) -> host uint8."""
+    t = t.detach().contiguous()
+    if t.dtype == torch.uint8:
+        return t.cpu().numpy()
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
 
 
 def compact_rows(k_pool: torch.Tensor, v_pool: torch.Tensor, table: np.ndarray, lens):

@@ -22,7 +22,8 @@ def _declared_functions():
 
 def _kv(**kw):
     d = dict(k_pool=FAKE, v_pool=FAKE, block_table=FAKE, num_pages=10, bt_stride=4,
-             num_kv_heads=2, page_size=16, head_dim=128)
+             num_kv_heads=2, page_size=16, head_dim=128, kv_dtype=_lib.RA_KV_BF16, k_scale=1.0,
+             v_scale=1.0)
     d.update(kw)
     return _lib.RaPagedKV(**d)
 
@@ -40,7 +41,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.ra_abi_version() == 1
+    assert lib.ra_abi_version() == 2
     assert lib.ra_status_string(0) == b"RA_OK"
     assert lib.ra_status_string(4) == b"RA_ERR_WORKSPACE"
     assert lib.ra_status_string(99) == b"RA_UNKNOWN_STATUS"
@@ -222,3 +223,22 @@ def test_mixed_validation(lib):
     # an empty side is not checked at all; both empty: no work, no launch
     assert _mixed(lib, None, None, Bd=0, Ba=0, qd=None, qa=None) == _lib.RA_OK
     assert _mixed(lib, kv, None, Bd=0, total_q=0, ws=None) == _lib.RA_OK
+
+
+def test_fp8_pool_validation(lib):
+    """fp8 pools: an unknown element type, bad scales, and the entry points that do not
+    take fp8 pools are rejected before any launch."""
+    fp8 = dict(kv_dtype=_lib.RA_KV_FP8_E4M3, k_scale=0.5, v_scale=2.0)
+    assert _decode(lib, _kv(kv_dtype=7)) == _lib.RA_ERR_UNSUPPORTED
+    for bad in (0.0, -1.0, float("inf"), float("nan")):
+        assert _decode(lib, _kv(**dict(fp8, k_scale=bad))) == _lib.RA_ERR_SHAPE
+        assert _decode(lib, _kv(**dict(fp8, v_scale=bad))) == _lib.RA_ERR_SHAPE
+    assert _decode(lib, _kv(**fp8), ws_bytes=16) == _lib.RA_ERR_WORKSPACE   # fp8 decode passes
+    assert _decode(lib, _kv(**fp8), B=0) == _lib.RA_OK
+    assert lib.rollout_attn_append(FAKE, FAKE, FAKE, ctypes.byref(_kv(**fp8)), 2, 4, 10, 5, 64,
+                                   0.1, FAKE, None, FAKE, 1 << 30, None) == _lib.RA_ERR_UNSUPPORTED
+    kv = _kv()
+    assert _mixed(lib, _kv(**fp8), kv) == _lib.RA_ERR_UNSUPPORTED
+    assert _mixed(lib, kv, _kv(**fp8)) == _lib.RA_ERR_UNSUPPORTED
+    # the bf16 scales are ignored
+    assert _decode(lib, _kv(k_scale=0.0, v_scale=float("nan")), B=0) == _lib.RA_OK
