@@ -27,6 +27,8 @@ unmasked query-key pairs, two matrix products each) is reported beside it.
 decode on one stream) beside its lower bounds at the published peaks, and the
 same step with decode and append rows in one persistent launch
 (`single_launch`).
+`append_write` times the append workload's page write + append as two calls
+and as one fused call.
 `fp8_kv_decode` times the decode workload over an fp8 (OCP E4M3) pool beside
 the bf16 pool (each alone).
 `shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
@@ -395,6 +397,48 @@ def fp8_kv_leg(ra, synth, dev, wd, td, steps: int, warmup: int):
     return res
 
 
+def append_write_leg(ra, dev, wa, ta, kv_aw, kv_a, steps: int, warmup: int):
+    """The append workload's page write + append as two calls and as one fused call
+    (rollout_attn_append_write), each timed alone."""
+    import torch
+
+    def i32(x):
+        return torch.as_tensor(np.ascontiguousarray(np.asarray(x, np.int32)), device=dev)
+
+    cu_q, ctx = i32(wa.cu_q()), i32(wa.ctx_lens)
+    max_q, max_kv = int(wa.q_lens.max()), int((wa.ctx_lens + wa.q_lens).max())
+    n = int(wa.q_lens.sum())
+    k_new, v_new = ta.k_new[-n:], ta.v_new[-n:]
+    out = torch.empty((n, wa.Hq, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty(ra.append_workspace_size(wa.q_lens.shape[0], wa.Hq, wa.Hkv, max_q),
+                     dtype=torch.uint8, device=dev)
+    calls = {
+        "separate": lambda: (ra.kv_page_write(k_new, v_new, cu_q, ctx, kv_aw, max_q, max_kv),
+                             ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv, SCALE,
+                                       out=out, workspace=ws)),
+        "fused": lambda: ra.append_write(ta.q_append, k_new, v_new, cu_q, ctx, kv_a, max_q,
+                                         max_kv, SCALE, out=out, workspace=ws),
+    }
+    ms = {}
+    for name, fn in calls.items():
+        for _ in range(warmup):
+            fn()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for e in ev:
+            e[0].record()
+            fn()
+            e[1].record()
+        torch.cuda.synchronize()
+        ms[name] = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    flops = append_flops(wa)
+    res = {"workload": wa.name, "steps": steps, "warmup": warmup,
+           "separate_ms": round(ms["separate"], 4), "fused_ms": round(ms["fused"], 4),
+           "speedup": round(ms["separate"] / ms["fused"], 4),
+           "fused_TFLOP_s": round(flops / (ms["fused"] * 1e-3) / 1e12, 1)}
+    del out, ws
+    return res
+
+
 def logprob_leg(ra, synth, dev, steps: int, warmup: int):
     """token_logprob on the Qwen3-8B LM head (V = 151936, D = 4096): a decode
     batch of 64 tokens (bound by reading W) and 1024 tokens (bound by the
@@ -443,6 +487,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-shared-prefix", action="store_true",
                     help="skip the shared-prefix decode leg (8 tasks x 8 rollouts)")
+    ap.add_argument("--no-append-write", action="store_true",
+                    help="skip the fused page write + append leg")
     ap.add_argument("--no-fp8", action="store_true",
                     help="skip the fp8 KV pool decode leg")
     ap.add_argument("--no-logprob", action="store_true",
@@ -559,6 +605,9 @@ def main():
     shared = None
     if not args.no_shared_prefix:
         shared = shared_prefix_leg(ra, synth, dev, args.steps, args.warmup)
+    append_write = None
+    if not args.no_append_write:
+        append_write = append_write_leg(ra, dev, wa, ta, kv_aw, kv_a, args.steps, args.warmup)
     fp8 = None
     if not args.no_fp8:
         fp8 = fp8_kv_leg(ra, synth, dev, wd, td, args.steps, args.warmup)
@@ -618,6 +667,7 @@ def main():
                             "traffic": measured_traffic("append")},
         "mixed_step": mixed,
         "shared_prefix_decode": shared,
+        "append_write": append_write,
         "fp8_kv_decode": fp8,
         "token_logprob": logprob,
         "cpu_baseline": cpu_dec,

@@ -60,8 +60,8 @@
  *                   infinities) saturate to +-448, NaN becomes 0x7F.
  *   fp8 pools are supported by kv_page_write (quantizing), kv_page_gather
  *   (codes copied out), rollout_attn_decode and
- *   rollout_attn_decode_shared_prefix; the other entry points return
- *   RA_ERR_UNSUPPORTED for them.
+ *   rollout_attn_decode_shared_prefix; the append entry points and the mixed
+ *   step return RA_ERR_UNSUPPORTED for them.
  */
 #ifndef ROLLOUT_ATTN_H
 #define ROLLOUT_ATTN_H
@@ -217,6 +217,31 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                         int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
                         float *lse, void *workspace, size_t workspace_bytes,
                         hipStream_t stream);
+
+/*
+ * Append with the page write fused in: writes the chunk's keys and values into
+ * the pages and computes the append attention in one launch (plus the
+ * planning kernel). Equivalent, bitwise, to kv_page_write(k_new, v_new, cu_q,
+ * start_pos = ctx_lens) followed by rollout_attn_append on the same stream
+ * (Sec. 3.3.3: each new observation is appended to the retained tokens and
+ * attended in the same step). The tiles read the chunk's own keys and values
+ * from k_new / v_new and each writes the tokens of its query block, so the
+ * new tokens are read and written once and no tile waits for another.
+ *
+ *   q, cu_q, ctx_lens, kv, B, Hq, total_q, max_q_len, max_kv_len, scale, out,
+ *   lse, workspace: as rollout_attn_append (same workspace size)
+ *   k_new, v_new  bf16 [total_q][Hkv][128]: the chunk tokens' keys and values,
+ *                 packed like q; token i of row b goes to position
+ *                 ctx_lens[b] + i
+ * Precondition (not checked): no row of the call reads, below its ctx, a page
+ * slot that another row of the call writes.
+ * Errors: as rollout_attn_append; RA_ERR_UNSUPPORTED for fp8 pools.
+ */
+int rollout_attn_append_write(const void *q, const void *k_new, const void *v_new,
+                              const int32_t *cu_q, const int32_t *ctx_lens, const ra_paged_kv *kv,
+                              int32_t B, int32_t Hq, int32_t total_q, int32_t max_q_len,
+                              int32_t max_kv_len, float scale, float *out, float *lse,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Mixed step: the attention of one rollout step in which some trajectories

@@ -24,7 +24,8 @@ from ._lib import RolloutAttnError  # noqa: F401  (re-export)
 PAGE_SIZE = 16
 HEAD_DIM = 128
 
-__all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "mixed", "kv_page_write",
+__all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "append_write", "mixed",
+           "kv_page_write",
            "kv_page_gather", "token_logprob", "decode_workspace_size",
            "decode_shared_prefix_workspace_size", "append_workspace_size", "mixed_workspace_size",
            "token_logprob_workspace_size", "abi_version", "RolloutAttnError"]
@@ -253,6 +254,56 @@ def append(q: torch.Tensor, cu_q: torch.Tensor, ctx_lens: torch.Tensor, kv: Page
         q.data_ptr(), cu_q.data_ptr(), ctx_lens.data_ptr(), ctypes.byref(s), B, Hq, total_q,
         max_q_len, max_kv_len, float(scale), out.data_ptr(), _ptr(lse), workspace.data_ptr(),
         workspace.numel(), _stream(dev, stream)))
+    return out, lse
+
+
+def append_write(q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, cu_q: torch.Tensor,
+                 ctx_lens: torch.Tensor, kv: PagedKV, max_q_len: Optional[int] = None,
+                 max_kv_len: Optional[int] = None, scale: Optional[float] = None,
+                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                 want_lse: bool = False, workspace: Optional[torch.Tensor] = None, stream=None
+                 ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Write the chunks' K/V (bf16 [total_q][Hkv][128], packed like q) at positions
+    ctx_lens[b] + i and run the append attention, in one launch."""
+    lib = _lib.load()
+    dev = kv.device
+    for t, n in ((q, "q"), (k_new, "k_new"), (v_new, "v_new")):
+        _need(t, n, torch.bfloat16, dev)
+    _need(cu_q, "cu_q", torch.int32, dev)
+    _need(ctx_lens, "ctx_lens", torch.int32, dev)
+    total_q, Hq, D = q.shape
+    _shape(q, (total_q, Hq, HEAD_DIM), "q")
+    _shape(k_new, (total_q, kv.num_kv_heads, HEAD_DIM), "k_new")
+    _shape(v_new, (total_q, kv.num_kv_heads, HEAD_DIM), "v_new")
+    B = ctx_lens.shape[0]
+    _shape(cu_q, (B + 1,), "cu_q")
+    _rows(kv, B)
+    if max_q_len is None or max_kv_len is None:
+        t = (cu_q[1:] - cu_q[:-1]) if B else cu_q[:0]
+        if max_q_len is None:
+            max_q_len = int(t.max().item()) if B else 0
+        if max_kv_len is None:
+            max_kv_len = int((t + ctx_lens).max().item()) if B else 0
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty((total_q, Hq, D), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, dev)
+    _shape(out, (total_q, Hq, HEAD_DIM), "out")
+    if lse is None and want_lse:
+        lse = torch.empty((total_q, Hq), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+        _shape(lse, (total_q, Hq), "lse")
+    ws_bytes = lib.rollout_attn_append_workspace_size(B, Hq, kv.num_kv_heads, max_q_len)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    _need(workspace, "workspace", torch.uint8, dev)
+    s = kv.struct()
+    _lib.check("rollout_attn_append_write", lib.rollout_attn_append_write(
+        q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), cu_q.data_ptr(), ctx_lens.data_ptr(),
+        ctypes.byref(s), B, Hq, total_q, max_q_len, max_kv_len, float(scale), out.data_ptr(),
+        _ptr(lse), workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
     return out, lse
 
 

@@ -24,6 +24,7 @@ EXPORTS = (
     "rollout_attn_decode_shared_prefix",
     "rollout_attn_append_workspace_size",
     "rollout_attn_append",
+    "rollout_attn_append_write",
     "rollout_attn_mixed_workspace_size",
     "rollout_attn_mixed",
     "kv_page_write",
@@ -88,6 +89,9 @@ def load() -> ctypes.CDLL:
     lib.rollout_attn_append.argtypes = [vp, vp, vp, kvp, i32, i32, i32, i32, i32, f32, vp, vp,
                                         vp, sz, vp]
     lib.rollout_attn_append.restype = ctypes.c_int
+    lib.rollout_attn_append_write.argtypes = [vp, vp, vp, vp, vp, kvp, i32, i32, i32, i32, i32,
+                                              f32, vp, vp, vp, sz, vp]
+    lib.rollout_attn_append_write.restype = ctypes.c_int
     lib.rollout_attn_mixed_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
     lib.rollout_attn_mixed_workspace_size.restype = sz
     lib.rollout_attn_mixed.argtypes = [vp, kvp, vp, i32, i32, vp, vp,

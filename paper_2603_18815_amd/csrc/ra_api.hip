@@ -159,6 +159,32 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                                      workspace, layout, stream));
 }
 
+int rollout_attn_append_write(const void *q, const void *k_new, const void *v_new,
+                              const int32_t *cu_q, const int32_t *ctx_lens, const ra_paged_kv *kv,
+                              int32_t B, int32_t Hq, int32_t total_q, int32_t max_q_len,
+                              int32_t max_kv_len, float scale, float *out, float *lse,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (B < 0 || Hq <= 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0) return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!q || !k_new || !v_new || !cu_q || !ctx_lens || !out) return RA_ERR_NULL;
+  if (is_fp8(kv)) return RA_ERR_UNSUPPORTED;
+  if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
+  if (Hq / kv->num_kv_heads > 256 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_kv_len) || max_q_len > max_kv_len) return RA_ERR_SHAPE;
+  if (B == 0 || total_q == 0 || max_q_len == 0) return RA_OK;
+  const ra::PagedKV k = to_internal(kv);
+  if (k.hkv > ra::mixed_hkv_limit()) return RA_ERR_UNSUPPORTED;
+  const ra::MixedLayout layout = ra::mixed_layout(0, B, Hq, k.hkv, k.hkv, 0, max_q_len);
+  if (layout.max_tiles > 0x7fffffff - 0xffff || layout.qblocks >= (1 << 23))
+    return RA_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < layout.bytes) return RA_ERR_WORKSPACE;
+  return hip_status(ra::launch_mixed(
+      nullptr, k, nullptr, 0, 0, nullptr, nullptr, static_cast<const uint16_t *>(q), cu_q,
+      ctx_lens, k, B, total_q, max_q_len, max_kv_len, out, lse, Hq, scale, workspace, layout,
+      stream, static_cast<const uint16_t *>(k_new), static_cast<const uint16_t *>(v_new)));
+}
+
 size_t rollout_attn_mixed_workspace_size(int32_t B_decode, int32_t B_append, int32_t Hq,
                                          int32_t Hkv_decode, int32_t Hkv_append,
                                          int32_t max_kv_len_decode, int32_t max_q_len) {

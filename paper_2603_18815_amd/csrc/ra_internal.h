@@ -75,7 +75,8 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
                         int32_t B_append, int32_t total_q, int32_t max_q_len,
                         int32_t max_kv_len_append, float *out_append, float *lse_append,
                         int32_t hq, float scale, void *workspace, const MixedLayout &layout,
-                        hipStream_t stream);
+                        hipStream_t stream, const uint16_t *k_new = nullptr,
+                        const uint16_t *v_new = nullptr);
 
 // ---- per-token log-probabilities under an LM head ----
 int32_t logprob_chunks(int32_t V);

@@ -50,6 +50,7 @@ struct MixedArgs {
   int32_t *header;  // per queue q: [q] next entry, [8+q] tiles, [16+q] splits,
                     // [24+q] tile segment start, [32+q] split segment start
   int32_t B_append, qblocks;
+  const uint16_t *k_new, *v_new;   // fused page write: the chunks' K / V (else null)
 };
 
 // Exclusive prefix sum of v over the kPlanThreads threads of the workgroup;
@@ -192,7 +193,8 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m) {
 }
 
 // kDecode: the call has decode rows (otherwise every entry is an append tile).
-template <bool kPosScale, bool kDecode>
+// kFused: the append tiles also write their chunk tokens into the pages.
+template <bool kPosScale, bool kDecode, bool kFused = false>
 __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
   __shared__ union {
     atile::AppendLds ap;
@@ -221,8 +223,9 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
                                                   e.y >> kHeadBits, e.x, lds.de);
       } else {
         const int2 e = tiles[j - dj];
-        atile::append_tile<kPosScale>(m.ap, e.y >> kHeadBits, e.y & ((1 << kHeadBits) - 1),
-                                      e.x, lds.ap);
+        atile::append_tile<kPosScale, kFused>(m.ap, e.y >> kHeadBits,
+                                              e.y & ((1 << kHeadBits) - 1), e.x, lds.ap,
+                                              m.k_new, m.v_new);
       }
     }
   }
@@ -258,11 +261,14 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
                         int32_t B_append, int32_t total_q, int32_t max_q_len,
                         int32_t max_kv_len_append, float *out_append, float *lse_append,
                         int32_t hq, float scale, void *workspace, const MixedLayout &layout,
-                        hipStream_t stream) {
+                        hipStream_t stream, const uint16_t *k_new, const uint16_t *v_new) {
   char *ws = static_cast<char *>(workspace);
   MixedArgs m;
   m.ap = atile::make_append_args(q_append, cu_q, ctx_lens, kv_append, hq, total_q, max_q_len,
                                  max_kv_len_append, scale, out_append, lse_append);
+  m.k_new = k_new;
+  m.v_new = v_new;
+  const bool fused = k_new != nullptr;   // append rows only
   m.de = dsplit::make_decode_args(q_decode, kv_decode, kv_lens, B_decode, hq,
                                   max_kv_len_decode, scale, ws + layout.partials_offset,
                                   layout.plan.max_splits, layout.plan);
@@ -287,7 +293,12 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   const unsigned grid = (unsigned)(entries < cus ? (entries > 0 ? entries : 1) : cus);
   const dim3 g(grid), b(kMixThreads);
   const bool pos = m.ap.scale_log2 > 0.f || B_append == 0;
-  if (B_decode == 0) {
+  if (B_decode == 0 && fused) {
+    if (pos)
+      hipLaunchKernelGGL((mixed_kernel<true, false, true>), g, b, 0, stream, m);
+    else
+      hipLaunchKernelGGL((mixed_kernel<false, false, true>), g, b, 0, stream, m);
+  } else if (B_decode == 0) {
     if (pos)
       hipLaunchKernelGGL((mixed_kernel<true, false>), g, b, 0, stream, m);
     else

@@ -242,3 +242,22 @@ def test_fp8_pool_validation(lib):
     assert _mixed(lib, kv, _kv(**fp8)) == _lib.RA_ERR_UNSUPPORTED
     # the bf16 scales are ignored
     assert _decode(lib, _kv(k_scale=0.0, v_scale=float("nan")), B=0) == _lib.RA_OK
+
+
+def test_append_write_validation(lib):
+    def call(kv, **kw):
+        d = dict(q=FAKE, k=FAKE, v=FAKE, cu=FAKE, ctx=FAKE, B=2, Hq=4, total_q=10, max_q=5,
+                 max_kv=64, out=FAKE, ws=FAKE, ws_bytes=1 << 30)
+        d.update(kw)
+        return lib.rollout_attn_append_write(d["q"], d["k"], d["v"], d["cu"], d["ctx"],
+                                             ctypes.byref(kv), d["B"], d["Hq"], d["total_q"],
+                                             d["max_q"], d["max_kv"], 0.1, d["out"], None,
+                                             d["ws"], d["ws_bytes"], None)
+    assert call(_kv(), k=None) == _lib.RA_ERR_NULL
+    assert call(_kv(), v=None) == _lib.RA_ERR_NULL
+    assert call(_kv(), max_kv=100) == _lib.RA_ERR_SHAPE
+    assert call(_kv(), Hq=5) == _lib.RA_ERR_SHAPE
+    assert call(_kv(kv_dtype=_lib.RA_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0)) == \
+        _lib.RA_ERR_UNSUPPORTED
+    assert call(_kv(), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
+    assert call(_kv(), total_q=0, ws=None) == _lib.RA_OK
