@@ -224,9 +224,10 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
  * planning kernel). Equivalent, bitwise, to kv_page_write(k_new, v_new, cu_q,
  * start_pos = ctx_lens) followed by rollout_attn_append on the same stream
  * (Sec. 3.3.3: each new observation is appended to the retained tokens and
- * attended in the same step). The tiles read the chunk's own keys and values
- * from k_new / v_new and each writes the tokens of its query block, so the
- * new tokens are read and written once and no tile waits for another.
+ * attended in the same step). The write runs inside the planning kernel's
+ * launch (its other workgroups write while one plans), so the call is two
+ * launches instead of the three of the separate calls; the attention kernel
+ * then reads the chunk from the pages.
  *
  *   q, cu_q, ctx_lens, kv, B, Hq, total_q, max_q_len, max_kv_len, scale, out,
  *   lse, workspace: as rollout_attn_append (same workspace size)

@@ -178,6 +178,9 @@ int rollout_attn_append_write(const void *q, const void *k_new, const void *v_ne
   const ra::MixedLayout layout = ra::mixed_layout(0, B, Hq, k.hkv, k.hkv, 0, max_q_len);
   if (layout.max_tiles > 0x7fffffff - 0xffff || layout.qblocks >= (1 << 23))
     return RA_ERR_UNSUPPORTED;
+  // the write runs as (row, page, head) blocks, four per workgroup
+  if ((int64_t)B * k.hkv * ((int64_t)max_q_len / RA_PAGE_SIZE + 2) / 4 > 0x7ffffff0)
+    return RA_ERR_UNSUPPORTED;
   if (!workspace || workspace_bytes < layout.bytes) return RA_ERR_WORKSPACE;
   return hip_status(ra::launch_mixed(
       nullptr, k, nullptr, 0, 0, nullptr, nullptr, static_cast<const uint16_t *>(q), cu_q,

@@ -46,8 +46,8 @@ constexpr float kSumLimit = 16384.f;                  // weight-sum bound betwee
 
 struct AppendArgs {
   const uint16_t *q;
-  uint16_t *k_pool;   // written only by the fused variant (the chunk's own tokens)
-  uint16_t *v_pool;
+  const uint16_t *k_pool;
+  const uint16_t *v_pool;
   const int32_t *block_table;
   const int32_t *cu_q;
   const int32_t *ctx_lens;
@@ -119,15 +119,9 @@ __device__ __forceinline__ int append_tile_blocks(const AppendArgs &a, const App
 
 // One tile: query block qblk of row b, KV head g, by a workgroup of kThreads
 // threads. Every thread of the workgroup calls it with the same arguments.
-// kFused: the chunk's keys and values are not in the pool yet; the tile reads
-// them from k_new / v_new (bf16 [total_q][Hkv][128], positions ctx and
-// beyond) and writes its own query block's tokens of head g into the pages.
-// No tile reads a pool slot that a tile of the same call writes, so the
-// tiles need no ordering.
-template <bool kPosScale, bool kFused = false>
+template <bool kPosScale>
 __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g, int b,
-                                            AppendLds &lds, const uint16_t *k_new = nullptr,
-                                            const uint16_t *v_new = nullptr) {
+                                            AppendLds &lds) {
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1), wave = tid / kWave;
   const int col = lane & 31, grp = lane >> 5;
@@ -180,25 +174,8 @@ __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g
       const int pgi = blk * kBlockPages + p * kPagesPerPass + st_page;
       const int id = clamp_page(pgi < row_pages ? bt[pgi] : bt[0], a.num_pages);
       const size_t base = ((size_t)id * a.hkv + g) * head_stride;
-      if (kFused && (pgi + 1) * kPage > ctx) {
-        // a page holding chunk tokens: those come from k_new / v_new (their
-        // index clamped into the chunk; positions past its end are masked)
-        const int pos = pgi * kPage + st_slot;
-        kreg[p] = pos >= ctx ? load_u32x4(k_new + ((size_t)(cu0 + min(pos - ctx, T - 1)) * a.hkv +
-                                                     g) * kHeadDim + st_kch * 8)
-                             : load_u32x4(a.k_pool + base + st_slot * kHeadDim + st_kch * 8);
-        auto v_elem = [&](int e) __attribute__((always_inline)) -> uint32_t {
-          const int vp = pgi * kPage + st_half * 8 + e;
-          return vp >= ctx ? v_new[((size_t)(cu0 + min(vp - ctx, T - 1)) * a.hkv + g) *
-                                         kHeadDim + st_d]
-                           : a.v_pool[base + st_d * kPage + st_half * 8 + e];
-        };
-#pragma unroll
-        for (int e = 0; e < 4; ++e) vreg[p][e] = v_elem(2 * e) | (v_elem(2 * e + 1) << 16);
-      } else {
-        kreg[p] = load_u32x4(a.k_pool + base + st_slot * kHeadDim + st_kch * 8);
-        vreg[p] = load_u32x4(a.v_pool + base + st_d * kPage + st_half * 8);
-      }
+      kreg[p] = load_u32x4(a.k_pool + base + st_slot * kHeadDim + st_kch * 8);
+      vreg[p] = load_u32x4(a.v_pool + base + st_d * kPage + st_half * 8);
     }
   };
   auto stage_store = [&](int blk, int buf) __attribute__((always_inline)) {
@@ -344,40 +321,6 @@ __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g
 
     if (blk + 1 < nblocks) stage_store(blk + 1, buf ^ 1);
     __syncthreads();
-  }
-
-  if constexpr (kFused) {
-    // this tile's tokens ctx + i0 .. ctx + i_end - 1 of KV head g into the pages
-    const int n = i_end - i0, q0 = ctx + i0;
-    for (int idx = tid; idx < n * 16; idx += kThreads) {   // K: 16 bytes per thread
-      const int t = idx >> 4, ch = idx & 15, pos = q0 + t;
-      const int id = clamp_page(bt[pos / kPage], a.num_pages);
-      store_u32x4(a.k_pool + ((size_t)id * a.hkv + g) * head_stride + (pos % kPage) * kHeadDim +
-                      ch * 8,
-                  load_u32x4(k_new + ((size_t)(cu0 + i0 + t) * a.hkv + g) * kHeadDim + ch * 8));
-    }
-    // V pages are [d][slot]: a thread writes the slots of one (page, d, 8-slot half)
-    const int p_first = q0 / kPage, p_last = (q0 + n - 1) / kPage;
-    const int items = (p_last - p_first + 1) * kHeadDim * 2;
-    for (int idx = tid; idx < items; idx += kThreads) {
-      const int pg = p_first + idx / (kHeadDim * 2), r = idx % (kHeadDim * 2);
-      const int d = r >> 1, s0 = pg * kPage + (r & 1) * 8;
-      const int lo = max(s0, q0), hi = min(s0 + 8, q0 + n);
-      if (lo >= hi) continue;
-      const int id = clamp_page(bt[pg], a.num_pages);
-      uint16_t *dst = a.v_pool + ((size_t)id * a.hkv + g) * head_stride + d * kPage + (r & 1) * 8;
-      auto src = [&](int pos) __attribute__((always_inline)) -> uint32_t {
-        return v_new[((size_t)(cu0 + pos - ctx) * a.hkv + g) * kHeadDim + d];
-      };
-      if (lo == s0 && hi == s0 + 8) {
-        u32x4 w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = src(s0 + 2 * e) | (src(s0 + 2 * e + 1) << 16);
-        store_u32x4(dst, w);
-      } else {
-        for (int pos = lo; pos < hi; ++pos) dst[pos - s0] = (uint16_t)src(pos);
-      }
-    }
   }
 
   // ---- epilogue: normalise and store; lane holds d = 32 dt + 8 (r/4) + 4 grp + r%4 ----

@@ -7,6 +7,7 @@
 // gather copies the codes out.
 #include "ra_device.h"
 #include "ra_internal.h"
+#include "ra_page_write.h"
 
 namespace ra {
 namespace {
@@ -14,53 +15,14 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kVPitch = kHeadDim + 8;  // LDS row pitch (elements) of the staged V slots
 
-__global__ __launch_bounds__(kThreads) void page_write_kernel(
-    const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
-    const int32_t *__restrict__ cu_new, const int32_t *__restrict__ start_pos,
-    uint16_t *__restrict__ k_pool, uint16_t *__restrict__ v_pool,
-    const int32_t *__restrict__ block_table, int bt_stride, int num_pages, int hkv,
-    int total_new, int max_new, int max_pos) {
-  const int chunk = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x;
-  // Row extent, clamped so that no access leaves the caller's arrays.
-  const int cu0 = min(max(cu_new[b], 0), total_new);
-  const int n = min(min(max(cu_new[b + 1] - cu0, 0), max_new), total_new - cu0);
-  if (n <= 0) return;
-  const int s = min(max(start_pos[b], 0), max_pos - n);
-  if (s < 0) return;
-  const int pg = s / kPage + chunk;                   // row-relative page
-  if (pg > (s + n - 1) / kPage) return;
-  const int lo = max(s, pg * kPage), hi = min(s + n, pg * kPage + kPage);
-  const int id = clamp_page(block_table[(size_t)b * bt_stride + pg], num_pages);
-
-  __shared__ uint16_t sv[kPage][kVPitch];
-  const int slot = tid >> 4, ch = tid & 15;            // token slot, 16-byte chunk
-  const int pos = pg * kPage + slot;
-  const bool live = pos >= lo && pos < hi;
-  if (live) {
-    const size_t src = ((size_t)(cu0 + pos - s) * hkv + g) * kHeadDim + ch * 8;
-    const size_t dst = (((size_t)id * hkv + g) * kPage + slot) * kHeadDim + ch * 8;
-    store_u32x4(k_pool + dst, load_u32x4(k_new + src));
-    *reinterpret_cast<u32x4 *>(&sv[slot][ch * 8]) = load_u32x4(v_new + src);
-  }
+// bf16 pools: one (row, page, KV head) block per workgroup.
+__global__ __launch_bounds__(pwrite::kItemThreads) void page_write_kernel(pwrite::WriteArgs a) {
+  const pwrite::WriteItem it = pwrite::write_item(a, blockIdx.x, blockIdx.z);
+  if (!it.active) return;
+  __shared__ uint16_t sv[kPage][pwrite::kVPitch];
+  pwrite::write_phase1(a, it, blockIdx.y, threadIdx.x, sv);
   __syncthreads();
-  // V page is [d][slot]: thread -> one d row, eight slots.
-  const int d = tid >> 1, s0 = (tid & 1) * 8;
-  uint16_t *dst = v_pool + (((size_t)id * hkv + g) * kHeadDim + d) * kPage + s0;
-  const int p0 = pg * kPage + s0;
-  if (p0 >= lo && p0 + 8 <= hi) {
-    uint16_t t[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) t[e] = sv[s0 + e][d];
-    u32x4 w;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)t[2 * e] | ((uint32_t)t[2 * e + 1] << 16);
-    store_u32x4(dst, w);
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (p0 + e >= lo && p0 + e < hi) dst[e] = sv[s0 + e][d];
-  }
+  pwrite::write_phase2(a, it, blockIdx.y, threadIdx.x, sv);
 }
 
 __global__ __launch_bounds__(kThreads) void page_gather_kernel(
@@ -189,9 +151,10 @@ hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const
                        kv.num_pages, kv.hkv, total_new, max_new, max_pos, 1.0f / kv.k_scale,
                        1.0f / kv.v_scale);
   else
-    hipLaunchKernelGGL(page_write_kernel, grid, dim3(kThreads), 0, stream, k_new, v_new, cu_new,
-                       start_pos, kv.k_pool, kv.v_pool, kv.block_table, kv.bt_stride,
-                       kv.num_pages, kv.hkv, total_new, max_new, max_pos);
+    hipLaunchKernelGGL(page_write_kernel, grid, dim3(pwrite::kItemThreads), 0, stream,
+                       pwrite::WriteArgs{k_new, v_new, cu_new, start_pos, kv.k_pool, kv.v_pool,
+                                         kv.block_table, kv.bt_stride, kv.num_pages, kv.hkv,
+                                         total_new, max_new, max_pos});
   return hipGetLastError();
 }
 

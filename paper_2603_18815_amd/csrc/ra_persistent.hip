@@ -29,6 +29,7 @@
 #include "ra_append_tile.h"
 #include "ra_decode_split.h"
 #include "ra_internal.h"
+#include "ra_page_write.h"
 
 namespace ra {
 namespace {
@@ -50,7 +51,6 @@ struct MixedArgs {
   int32_t *header;  // per queue q: [q] next entry, [8+q] tiles, [16+q] splits,
                     // [24+q] tile segment start, [32+q] split segment start
   int32_t B_append, qblocks;
-  const uint16_t *k_new, *v_new;   // fused page write: the chunks' K / V (else null)
 };
 
 // Exclusive prefix sum of v over the kPlanThreads threads of the workgroup;
@@ -82,7 +82,29 @@ __device__ __forceinline__ int row_qblocks(const atile::AppendArgs &ap, const at
   return (r.T + ap.q_per_block - 1) / ap.q_per_block;
 }
 
-__global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m) {
+// Workgroup 0 plans. With the page write fused in (write_chunks > 0), every
+// other workgroup writes four (row, page, KV head) blocks of the chunks' K/V
+// meanwhile; the attention kernel after this one reads them from the pool.
+__global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m, pwrite::WriteArgs w,
+                                                                  int32_t write_chunks) {
+  if (blockIdx.x > 0) {
+    constexpr int kPer = kPlanThreads / pwrite::kItemThreads;
+    __shared__ uint16_t sv[kPer][kPage][pwrite::kVPitch];
+    const int part = threadIdx.x / pwrite::kItemThreads, t = threadIdx.x % pwrite::kItemThreads;
+    const int64_t item = (int64_t)(blockIdx.x - 1) * kPer + part;   // (row, head, page)
+    pwrite::WriteItem it;
+    it.active = false;
+    int g = 0;
+    if (item < (int64_t)m.B_append * w.hkv * write_chunks) {
+      const int64_t bg = item / write_chunks;
+      g = (int)(bg % w.hkv);
+      it = pwrite::write_item(w, (int)(item % write_chunks), (int)(bg / w.hkv));
+    }
+    if (it.active) pwrite::write_phase1(w, it, g, t, sv[part]);
+    __syncthreads();
+    if (it.active) pwrite::write_phase2(w, it, g, t, sv[part]);
+    return;
+  }
   __shared__ int count[kCostBuckets];   // rows per key-block count, then write cursors
   __shared__ int s_scan[kPlanThreads];
   __shared__ int s_total;
@@ -193,8 +215,7 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m) {
 }
 
 // kDecode: the call has decode rows (otherwise every entry is an append tile).
-// kFused: the append tiles also write their chunk tokens into the pages.
-template <bool kPosScale, bool kDecode, bool kFused = false>
+template <bool kPosScale, bool kDecode>
 __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
   __shared__ union {
     atile::AppendLds ap;
@@ -223,9 +244,8 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
                                                   e.y >> kHeadBits, e.x, lds.de);
       } else {
         const int2 e = tiles[j - dj];
-        atile::append_tile<kPosScale, kFused>(m.ap, e.y >> kHeadBits,
-                                              e.y & ((1 << kHeadBits) - 1), e.x, lds.ap,
-                                              m.k_new, m.v_new);
+        atile::append_tile<kPosScale>(m.ap, e.y >> kHeadBits, e.y & ((1 << kHeadBits) - 1),
+                                      e.x, lds.ap);
       }
     }
   }
@@ -266,9 +286,6 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   MixedArgs m;
   m.ap = atile::make_append_args(q_append, cu_q, ctx_lens, kv_append, hq, total_q, max_q_len,
                                  max_kv_len_append, scale, out_append, lse_append);
-  m.k_new = k_new;
-  m.v_new = v_new;
-  const bool fused = k_new != nullptr;   // append rows only
   m.de = dsplit::make_decode_args(q_decode, kv_decode, kv_lens, B_decode, hq,
                                   max_kv_len_decode, scale, ws + layout.partials_offset,
                                   layout.plan.max_splits, layout.plan);
@@ -279,7 +296,16 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   m.B_append = B_append;
   m.qblocks = layout.qblocks;
 
-  hipLaunchKernelGGL(mixed_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, m);
+  // the fused page write (append rows only): the chunks' tokens at ctx_lens
+  pwrite::WriteArgs w{k_new,         v_new,          cu_q,        ctx_lens,
+                      kv_append.k_pool, kv_append.v_pool, kv_append.block_table,
+                      kv_append.bt_stride, kv_append.num_pages, kv_append.hkv,
+                      total_q,       max_q_len,      max_kv_len_append};
+  const int32_t write_chunks = k_new ? (max_q_len + kPage - 1) / kPage + 1 : 0;
+  const int64_t write_blocks =
+      ((int64_t)B_append * kv_append.hkv * write_chunks + 3) / (kPlanThreads / pwrite::kItemThreads);
+  hipLaunchKernelGGL(mixed_plan_kernel, dim3((unsigned)(1 + write_blocks)), dim3(kPlanThreads), 0,
+                     stream, m, w, write_chunks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // One workgroup per CU: the kernel's registers allow one 8-wave
@@ -293,12 +319,7 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   const unsigned grid = (unsigned)(entries < cus ? (entries > 0 ? entries : 1) : cus);
   const dim3 g(grid), b(kMixThreads);
   const bool pos = m.ap.scale_log2 > 0.f || B_append == 0;
-  if (B_decode == 0 && fused) {
-    if (pos)
-      hipLaunchKernelGGL((mixed_kernel<true, false, true>), g, b, 0, stream, m);
-    else
-      hipLaunchKernelGGL((mixed_kernel<false, false, true>), g, b, 0, stream, m);
-  } else if (B_decode == 0) {
+  if (B_decode == 0) {
     if (pos)
       hipLaunchKernelGGL((mixed_kernel<true, false>), g, b, 0, stream, m);
     else
