@@ -29,8 +29,8 @@ same step with decode and append rows in one persistent launch
 (`single_launch`).
 `append_write` times the append workload's page write + append as two calls
 and as one fused call.
-`fp8_kv_decode` times the decode workload over an fp8 (OCP E4M3) pool beside
-the bf16 pool (each alone).
+`fp8_kv_decode` times the decode workload (and the append workload) over fp8
+(OCP E4M3) pools beside the bf16 pools (each alone).
 `shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
 rollouts whose rows share each task's prompt pages. `token_logprob` times the
 fused LM-head log-probability kernel at the Qwen3-8B head for 64 and 1024
@@ -348,9 +348,9 @@ def fp8_decode_bytes(w) -> int:
     return int(per_row.sum())
 
 
-def fp8_kv_leg(ra, synth, dev, wd, td, steps: int, warmup: int):
-    """Decode of the B = 64 decode workload over an fp8 (E4M3) pool beside the same
-    rows over the bf16 pool, each timed alone."""
+def fp8_kv_leg(ra, synth, dev, wd, td, wa, ta, steps: int, warmup: int):
+    """Decode of the B = 64 decode workload, and append of the B = 32 append workload,
+    over fp8 (E4M3) pools beside the same rows over the bf16 pools, each timed alone."""
     import torch
 
     def i32(x):
@@ -368,10 +368,27 @@ def fp8_kv_leg(ra, synth, dev, wd, td, steps: int, warmup: int):
     out = torch.empty((B, wd.Hq, 128), dtype=torch.float32, device=dev)
     ws = torch.empty(ra.decode_workspace_size(B, wd.Hq, wd.Hkv, max_kv), dtype=torch.uint8,
                      device=dev)
+    na = wa.layout.num_pages
+    ka8 = synth.randn_fp8_codes((na, wa.Hkv, 16, 128), gen, dev, ks)
+    va8 = synth.randn_fp8_codes((na, wa.Hkv, 128, 16), gen, dev, vs)
+    bta = i32(wa.append_table())
+    kva8 = ra.PagedKV(ka8, va8, bta, ks, vs)
+    kva16 = ra.PagedKV(ta.k_pool, ta.v_pool, bta)
+    cu_q, ctx = i32(wa.cu_q()), i32(wa.ctx_lens)
+    max_q, max_kva = int(wa.q_lens.max()), int((wa.ctx_lens + wa.q_lens).max())
+    out_a = torch.empty((int(wa.q_lens.sum()), wa.Hq, 128), dtype=torch.float32, device=dev)
+    ws_a = torch.empty(ra.append_workspace_size(wa.q_lens.shape[0], wa.Hq, wa.Hkv, max_q),
+                       dtype=torch.uint8, device=dev)
     ms = {}
-    for name, kv in (("bf16", kv16), ("fp8", kv8)):
-        def fn():
-            ra.decode(td.q_decode, kv, lens, max_kv, SCALE, out=out, workspace=ws)
+    calls = [("bf16", lambda: ra.decode(td.q_decode, kv16, lens, max_kv, SCALE, out=out,
+                                        workspace=ws)),
+             ("fp8", lambda: ra.decode(td.q_decode, kv8, lens, max_kv, SCALE, out=out,
+                                       workspace=ws)),
+             ("append_bf16", lambda: ra.append(ta.q_append, cu_q, ctx, kva16, max_q, max_kva,
+                                               SCALE, out=out_a, workspace=ws_a)),
+             ("append_fp8", lambda: ra.append(ta.q_append, cu_q, ctx, kva8, max_q, max_kva,
+                                              SCALE, out=out_a, workspace=ws_a))]
+    for name, fn in calls:
         for _ in range(warmup):
             fn()
         ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
@@ -391,8 +408,12 @@ def fp8_kv_leg(ra, synth, dev, wd, td, steps: int, warmup: int):
         "fp8_GB_s": round(b8 / (ms["fp8"] * 1e-3) / 1e9, 1),
         "fp8_frac_hbm_peak": round(b8 / (ms["fp8"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "bf16_GB_s": round(b16 / (ms["bf16"] * 1e-3) / 1e9, 1),
+        "append_workload": wa.name,
+        "append_bf16_ms": round(ms["append_bf16"], 4),
+        "append_fp8_ms": round(ms["append_fp8"], 4),
+        "append_fp8_TFLOP_s": round(append_flops(wa) / (ms["append_fp8"] * 1e-3) / 1e12, 1),
     }
-    del k8, v8, out, ws
+    del k8, v8, out, ws, ka8, va8, out_a, ws_a
     torch.cuda.empty_cache()
     return res
 
@@ -610,7 +631,7 @@ def main():
         append_write = append_write_leg(ra, dev, wa, ta, kv_aw, kv_a, args.steps, args.warmup)
     fp8 = None
     if not args.no_fp8:
-        fp8 = fp8_kv_leg(ra, synth, dev, wd, td, args.steps, args.warmup)
+        fp8 = fp8_kv_leg(ra, synth, dev, wd, td, wa, ta, args.steps, args.warmup)
     logprob = None
     if not args.no_logprob:
         logprob = logprob_leg(ra, synth, dev, args.steps, args.warmup)

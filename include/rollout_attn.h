@@ -58,10 +58,11 @@
  *                   value x is stored as encode(fp32(x) * fp32(1 / scale)):
  *                   round to nearest even, magnitudes beyond 448 (and
  *                   infinities) saturate to +-448, NaN becomes 0x7F.
- *   fp8 pools are supported by kv_page_write (quantizing), kv_page_gather
- *   (codes copied out), rollout_attn_decode and
- *   rollout_attn_decode_shared_prefix; the append entry points and the mixed
- *   step return RA_ERR_UNSUPPORTED for them.
+ *   fp8 pools are supported by every entry point except
+ *   rollout_attn_append_write (RA_ERR_UNSUPPORTED); kv_page_write quantizes,
+ *   kv_page_gather copies the codes out, the attention entry points convert
+ *   the codes exactly to bf16 operands. A mixed call takes one element type
+ *   for both sides (RA_ERR_UNSUPPORTED otherwise).
  */
 #ifndef ROLLOUT_ATTN_H
 #define ROLLOUT_ATTN_H

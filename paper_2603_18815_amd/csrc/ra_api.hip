@@ -142,7 +142,6 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
   int s = check_kv(kv);
   if (s != RA_OK) return s;
   if (!q || !cu_q || !ctx_lens || !out) return RA_ERR_NULL;
-  if (is_fp8(kv)) return RA_ERR_UNSUPPORTED;
   if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
   if (Hq / kv->num_kv_heads > 256 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
   if (!positions_fit(kv, max_kv_len) || max_q_len > max_kv_len) return RA_ERR_SHAPE;
@@ -220,7 +219,6 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
   if (dec) {
     if ((s = check_kv(kv_decode)) != RA_OK) return s;
     if (!q_decode || !kv_lens || !out_decode) return RA_ERR_NULL;
-    if (is_fp8(kv_decode)) return RA_ERR_UNSUPPORTED;
     if (Hq % kv_decode->num_kv_heads != 0) return RA_ERR_SHAPE;
     if (Hq / kv_decode->num_kv_heads > 16 || B_decode > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
     if (!positions_fit(kv_decode, max_kv_len_decode)) return RA_ERR_SHAPE;
@@ -228,13 +226,14 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
   if (app) {
     if ((s = check_kv(kv_append)) != RA_OK) return s;
     if (!q_append || !cu_q || !ctx_lens || !out_append) return RA_ERR_NULL;
-    if (is_fp8(kv_append)) return RA_ERR_UNSUPPORTED;
     if (Hq % kv_append->num_kv_heads != 0) return RA_ERR_SHAPE;
     if (Hq / kv_append->num_kv_heads > 256) return RA_ERR_UNSUPPORTED;
     if (!positions_fit(kv_append, max_kv_len_append) || max_q_len > max_kv_len_append)
       return RA_ERR_SHAPE;
   }
   if (!dec && !app) return RA_OK;
+  // one element type per call (the kernel is built for one)
+  if (dec && app && is_fp8(kv_decode) != is_fp8(kv_append)) return RA_ERR_UNSUPPORTED;
   // an empty side borrows the other side's cache descriptor (never read)
   const ra::PagedKV kd = to_internal(dec ? kv_decode : kv_append);
   const ra::PagedKV ka = to_internal(app ? kv_append : kv_decode);

@@ -54,7 +54,8 @@ struct AppendArgs {
   float *out;
   float *lse;
   int32_t hq, hkv, group, bt_stride, num_pages, total_q, max_q_len, max_kv_len, q_per_block;
-  float scale_log2;
+  float scale_log2;   // softmax scale * log2(e) (* k_scale for fp8 pools)
+  float v_scale;      // multiplies the output (fp8 pools; 1 for bf16)
 };
 
 // D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16). Lane l supplies A row
@@ -119,7 +120,9 @@ __device__ __forceinline__ int append_tile_blocks(const AppendArgs &a, const App
 
 // One tile: query block qblk of row b, KV head g, by a workgroup of kThreads
 // threads. Every thread of the workgroup calls it with the same arguments.
-template <bool kPosScale>
+// kFp8: the pools hold E4M3 codes; the staging converts them exactly to bf16
+// on their way into LDS, so everything after the staging is the bf16 tile.
+template <bool kPosScale, bool kFp8 = false>
 __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g, int b,
                                             AppendLds &lds) {
   const int tid = threadIdx.x;
@@ -168,7 +171,22 @@ __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g
   const int st_slot = st_chunk >> 4, st_kch = st_chunk & 15;   // K: slot, 16-B chunk
   const int st_d = st_chunk >> 1, st_half = st_chunk & 1;      // V: dim row, 8-slot half
   u32x4 kreg[kPasses], vreg[kPasses];
+  // fp8 pools (2 KiB per page and head): one pass covers the block; thread
+  // -> page tid / 128 (wave-uniform), K: slot and 16-dim chunk, V: one dim
+  // row (all 16 slots).
+  const int f_page = __builtin_amdgcn_readfirstlane(tid >> 7), f_idx = tid & 127;
+  const int f_slot = f_idx >> 3, f_c16 = f_idx & 7;
   auto stage_load = [&](int blk) __attribute__((always_inline)) {
+    if constexpr (kFp8) {
+      const int pgi = blk * kBlockPages + f_page;
+      const int id = clamp_page(pgi < row_pages ? bt[pgi] : bt[0], a.num_pages);
+      const size_t base = ((size_t)id * a.hkv + g) * head_stride;   // bytes
+      kreg[0] = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint8_t *>(a.k_pool) +
+                                                 base + f_slot * kHeadDim + f_c16 * 16);
+      vreg[0] = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint8_t *>(a.v_pool) +
+                                                 base + f_idx * kPage);
+      return;
+    }
 #pragma unroll
     for (int p = 0; p < kPasses; ++p) {
       const int pgi = blk * kBlockPages + p * kPagesPerPass + st_page;
@@ -179,6 +197,26 @@ __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g
     }
   };
   auto stage_store = [&](int blk, int buf) __attribute__((always_inline)) {
+    if constexpr (kFp8) {
+      const int pos0 = (blk * kBlockPages + f_page) * kPage;
+      const bf16x8 k0 = fp8x8_to_bf16x8(u32x2{kreg[0][0], kreg[0][1]});
+      const bf16x8 k1 = fp8x8_to_bf16x8(u32x2{kreg[0][2], kreg[0][3]});
+      bf16x8 v0 = fp8x8_to_bf16x8(u32x2{vreg[0][0], vreg[0][1]});   // slots 0..7
+      bf16x8 v1 = fp8x8_to_bf16x8(u32x2{vreg[0][2], vreg[0][3]});   // slots 8..15
+      if (pos0 + kPage > row_end) {   // V slots past the row's end become zeros
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          v0[e] = pos0 + e < row_end ? v0[e] : (__bf16)0.f;
+          v1[e] = pos0 + 8 + e < row_end ? v1[e] : (__bf16)0.f;
+        }
+      }
+      uint16_t *kd = &sK[buf * kKBlockElems + k_lds(f_page * kPage + f_slot, 2 * f_c16)];
+      *reinterpret_cast<bf16x8 *>(kd) = k0;
+      *reinterpret_cast<bf16x8 *>(kd + 8) = k1;
+      *reinterpret_cast<bf16x8 *>(&sV[buf * kBlockElems + v_lds(f_page, f_idx, 0)]) = v0;
+      *reinterpret_cast<bf16x8 *>(&sV[buf * kBlockElems + v_lds(f_page, f_idx, 1)]) = v1;
+      return;
+    }
 #pragma unroll
     for (int p = 0; p < kPasses; ++p) {
       const int j = p * kPagesPerPass + st_page;        // page in the block
@@ -327,7 +365,7 @@ __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g
   const float l = l_run + __shfl_xor(l_run, 32);
   if (qpos >= 0) {
     const size_t row = (size_t)(cu0 + i0 + qi) * a.hq + (size_t)g * G + hh;
-    const float inv = 1.f / l;
+    const float inv = (kFp8 ? a.v_scale : 1.f) / l;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -364,7 +402,8 @@ inline AppendArgs make_append_args(const uint16_t *q, const int32_t *cu_q,
   a.max_q_len = max_q_len;
   a.max_kv_len = max_kv_len;
   a.q_per_block = kRowsPerGroup / a.group;
-  a.scale_log2 = scale * kLog2e;
+  a.scale_log2 = scale * kLog2e * kv.k_scale;
+  a.v_scale = kv.v_scale;
   return a;
 }
 

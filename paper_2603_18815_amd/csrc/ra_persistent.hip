@@ -215,7 +215,8 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m, p
 }
 
 // kDecode: the call has decode rows (otherwise every entry is an append tile).
-template <bool kPosScale, bool kDecode>
+// kFp8: the pools hold E4M3 codes.
+template <bool kPosScale, bool kDecode, bool kFp8>
 __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
   __shared__ union {
     atile::AppendLds ap;
@@ -240,12 +241,12 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
       const int dj = (int)((int64_t)j * nd / n);
       if (kDecode && (int)(((int64_t)j + 1) * nd / n) > dj) {
         const int2 e = splits[dj];
-        dsplit::decode_split<1, false, kMixWaves>(m.de, e.y & ((1 << kHeadBits) - 1),
-                                                  e.y >> kHeadBits, e.x, lds.de);
+        dsplit::decode_split<1, false, kMixWaves, kFp8>(m.de, e.y & ((1 << kHeadBits) - 1),
+                                                        e.y >> kHeadBits, e.x, lds.de);
       } else {
         const int2 e = tiles[j - dj];
-        atile::append_tile<kPosScale>(m.ap, e.y >> kHeadBits, e.y & ((1 << kHeadBits) - 1),
-                                      e.x, lds.ap);
+        atile::append_tile<kPosScale, kFp8>(m.ap, e.y >> kHeadBits,
+                                            e.y & ((1 << kHeadBits) - 1), e.x, lds.ap);
       }
     }
   }
@@ -319,16 +320,22 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   const unsigned grid = (unsigned)(entries < cus ? (entries > 0 ? entries : 1) : cus);
   const dim3 g(grid), b(kMixThreads);
   const bool pos = m.ap.scale_log2 > 0.f || B_append == 0;
-  if (B_decode == 0) {
-    if (pos)
-      hipLaunchKernelGGL((mixed_kernel<true, false>), g, b, 0, stream, m);
-    else
-      hipLaunchKernelGGL((mixed_kernel<false, false>), g, b, 0, stream, m);
-  } else {
-    if (pos)
-      hipLaunchKernelGGL((mixed_kernel<true, true>), g, b, 0, stream, m);
-    else
-      hipLaunchKernelGGL((mixed_kernel<false, true>), g, b, 0, stream, m);
+  const bool fp8 = kv_decode.fp8 || kv_append.fp8;   // the ABI layer allows one element type
+  const int variant = (pos ? 4 : 0) | (B_decode > 0 ? 2 : 0) | (fp8 ? 1 : 0);
+  switch (variant) {
+#define RA_MIXED_CASE(V, P, D, F)                                                       \
+  case V:                                                                               \
+    hipLaunchKernelGGL((mixed_kernel<P, D, F>), g, b, 0, stream, m);                    \
+    break;
+    RA_MIXED_CASE(0, false, false, false)
+    RA_MIXED_CASE(1, false, false, true)
+    RA_MIXED_CASE(2, false, true, false)
+    RA_MIXED_CASE(3, false, true, true)
+    RA_MIXED_CASE(4, true, false, false)
+    RA_MIXED_CASE(5, true, false, true)
+    RA_MIXED_CASE(6, true, true, false)
+    RA_MIXED_CASE(7, true, true, true)
+#undef RA_MIXED_CASE
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (B_decode == 0) return hipSuccess;

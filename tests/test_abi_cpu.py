@@ -235,11 +235,14 @@ def test_fp8_pool_validation(lib):
         assert _decode(lib, _kv(**dict(fp8, v_scale=bad))) == _lib.RA_ERR_SHAPE
     assert _decode(lib, _kv(**fp8), ws_bytes=16) == _lib.RA_ERR_WORKSPACE   # fp8 decode passes
     assert _decode(lib, _kv(**fp8), B=0) == _lib.RA_OK
+    # fp8 append passes the element-type check (and fails on the workspace here)
     assert lib.rollout_attn_append(FAKE, FAKE, FAKE, ctypes.byref(_kv(**fp8)), 2, 4, 10, 5, 64,
-                                   0.1, FAKE, None, FAKE, 1 << 30, None) == _lib.RA_ERR_UNSUPPORTED
+                                   0.1, FAKE, None, FAKE, 16, None) == _lib.RA_ERR_WORKSPACE
     kv = _kv()
+    # a mixed call takes one element type for both sides
     assert _mixed(lib, _kv(**fp8), kv) == _lib.RA_ERR_UNSUPPORTED
     assert _mixed(lib, kv, _kv(**fp8)) == _lib.RA_ERR_UNSUPPORTED
+    assert _mixed(lib, _kv(**fp8), _kv(**fp8), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
     # the bf16 scales are ignored
     assert _decode(lib, _kv(k_scale=0.0, v_scale=float("nan")), B=0) == _lib.RA_OK
 

@@ -174,3 +174,64 @@ def test_fp8_decode_qwen3_workload_sampled(device):
     sel = torch.as_tensor(rows, device=device)
     assert_attn_close(out[sel].cpu().numpy(), ref, "fp8 decode workload 2 sampled")
     np.testing.assert_allclose(lse[sel].cpu().numpy(), ref_lse, atol=1e-4, rtol=0)
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(32, 8), (16, 1), (64, 8)])
+def test_fp8_append_vs_oracle(device, Hq, Hkv):
+    ctx = [0, 1, 15, 16, 17, 100, 300, 2000]
+    T = [5, 64, 1, 63, 65, 200, 130, 17]
+    ks, vs = 2.0 ** -5, 0.04
+    say(f"fp8 append Hq={Hq} Hkv={Hkv}")
+    lay, k, v, gen = fp8_pool(Hq * 5 + Hkv, [c + t for c, t in zip(ctx, T)], Hkv, device, ks)
+    cu = np.concatenate([[0], np.cumsum(T)]).astype(np.int32)
+    q = synth.randn_bf16((int(cu[-1]), Hq, 128), gen, device)
+    kv = ra.PagedKV(k, v, i32(lay.block_table, device), ks, vs)
+    out, lse = ra.append(q, i32(cu, device), i32(ctx, device), kv, max(T),
+                         max(c + t for c, t in zip(ctx, T)), SCALE, want_lse=True)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.append_fp8(bits(q), cu, ctx, bits(k), bits(v), ks, vs,
+                                     lay.block_table, SCALE)
+    assert_attn_close(out.cpu().numpy(), ref, f"fp8 append G={Hq // Hkv}")
+    np.testing.assert_allclose(lse.cpu().numpy(), ref_lse, atol=2e-3, rtol=0)
+
+
+def test_fp8_append_poison_invisible(device):
+    ctx, T = [0, 17, 250, 1000], [33, 100, 64, 7]
+    lay, k, v, gen = fp8_pool(77, [c + t for c, t in zip(ctx, T)], 8, device, 0.05)
+    cu = np.concatenate([[0], np.cumsum(T)]).astype(np.int32)
+    q = synth.randn_bf16((int(cu[-1]), 32, 128), gen, device)
+    kv = ra.PagedKV(k, v, i32(lay.block_table, device), 0.05, 0.2)
+    args = (q, i32(cu, device), i32(ctx, device), kv, max(T), 1007, SCALE)
+    a, la = ra.append(*args, want_lse=True)
+    synth.poison_unowned(k, v, lay)
+    b, lb = ra.append(*args, want_lse=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(la, lb)
+
+
+def test_fp8_mixed_step_vs_oracle(device):
+    """Decode rows and append rows of one step over one fp8 pool, in one launch."""
+    w = synth.mixed_workload(31, 24, 32, 8, 0.35,
+                             lambda r, n: synth.uniform_int(r, n, 0, 1500),
+                             lambda r, n: synth.uniform_int(r, n, 1, 300), "small fp8 mixed")
+    ks, vs = 2.0 ** -5, 0.05
+    gen = synth.value_generator(31, device)
+    k = synth.randn_fp8_codes((w.layout.num_pages, 8, 16, 128), gen, device, ks)
+    v = synth.randn_fp8_codes((w.layout.num_pages, 8, 128, 16), gen, device, ks)
+    qd = synth.randn_bf16((w.kv_lens.size, 32, 128), gen, device)
+    qa = synth.randn_bf16((int(w.q_lens.sum()), 32, 128), gen, device)
+    kd = ra.PagedKV(k, v, i32(w.decode_table(), device), ks, vs)
+    ka = ra.PagedKV(k, v, i32(w.append_table(), device), ks, vs)
+    mq, mka = int(w.q_lens.max()), int((w.ctx_lens + w.q_lens).max())
+    od, oa, ld, la = ra.mixed(qd, kd, i32(w.kv_lens, device), qa, i32(w.cu_q(), device),
+                              i32(w.ctx_lens, device), ka, int(w.kv_lens.max()), mq, mka, SCALE,
+                              want_lse=True)
+    sa, _ = ra.append(qa, i32(w.cu_q(), device), i32(w.ctx_lens, device), ka, mq, mka, SCALE)
+    torch.cuda.synchronize()
+    assert torch.equal(oa, sa), "fp8 mixed append part differs from append()"
+    ref_d, _ = oracle.decode_fp8(bits(qd), bits(k), bits(v), ks, vs, w.decode_table(),
+                                 w.kv_lens, SCALE)
+    assert_attn_close(od.cpu().numpy(), ref_d, "fp8 mixed decode rows")
+    ref_a, _ = oracle.append_fp8(bits(qa), w.cu_q(), w.ctx_lens, bits(k), bits(v), ks, vs,
+                                 w.append_table(), SCALE)
+    assert_attn_close(oa.cpu().numpy(), ref_a, "fp8 mixed append rows")
