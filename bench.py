@@ -34,7 +34,7 @@ and as one fused call.
 `shared_prefix_decode` times plain and shared-prefix decode of 8 tasks x 8
 rollouts whose rows share each task's prompt pages. `token_logprob` times the
 fused LM-head log-probability kernel at the Qwen3-8B head for 64 and 1024
-tokens.
+tokens, with the head row-major and packed.
 `cpu_baseline` is the fp64 CPU oracle on a bounded sample of the same inputs.
 """
 import argparse
@@ -463,37 +463,47 @@ def append_write_leg(ra, dev, wa, ta, kv_aw, kv_a, steps: int, warmup: int):
 def logprob_leg(ra, synth, dev, steps: int, warmup: int):
     """token_logprob on the Qwen3-8B LM head (V = 151936, D = 4096): a decode
     batch of 64 tokens (bound by reading W) and 1024 tokens (bound by the
-    products)."""
+    products), with W row-major and packed (token_logprob_packed; the one-time
+    packing is timed on its own)."""
     import torch
 
     V, D = 151936, 4096
     gen = synth.value_generator(7, dev)
     W = (synth.randn_bf16((V, D), gen, dev).float() * (1.0 / math.sqrt(D))).to(torch.bfloat16)
+    Wp = ra.token_logprob_pack_weight(W)
     res = {"workload": f"token log-probabilities, LM head V={V} D={D} (Qwen3-8B), bf16"}
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for e in ev:
+            e[0].record()
+            fn()
+            e[1].record()
+        torch.cuda.synchronize()
+        return float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+
+    res["pack_ms"] = round(timed(lambda: ra.token_logprob_pack_weight(W, out=Wp)), 4)
     for N in (64, 1024):
         h = synth.randn_bf16((N, D), gen, dev)
         t = torch.randint(0, V, (N,), dtype=torch.int32, device=dev, generator=gen)
         out = torch.empty(N, dtype=torch.float32, device=dev)
         ws = torch.empty(ra.token_logprob_workspace_size(N, V), dtype=torch.uint8, device=dev)
-        for _ in range(warmup):
-            ra.token_logprob(h, W, t, 1.0, out=out, workspace=ws)
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
-        for e in ev:
-            e[0].record()
-            ra.token_logprob(h, W, t, 1.0, out=out, workspace=ws)
-            e[1].record()
-        torch.cuda.synchronize()
-        ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
         nbytes = V * D * 2 + N * D * 2 + N * 8
         flops = 2 * N * V * D
-        gbs, tfs = nbytes / (ms * 1e-3) / 1e9, flops / (ms * 1e-3) / 1e12
-        res[f"N{N}"] = {"ms": round(ms, 4), "algorithmic_bytes": nbytes,
+        for key, fn in ((f"N{N}", lambda: ra.token_logprob(h, W, t, 1.0, out=out, workspace=ws)),
+                        (f"N{N}_packed", lambda: ra.token_logprob_packed(
+                            h, Wp, V, t, 1.0, out=out, workspace=ws))):
+            ms = timed(fn)
+            gbs, tfs = nbytes / (ms * 1e-3) / 1e9, flops / (ms * 1e-3) / 1e12
+            res[key] = {"ms": round(ms, 4), "algorithmic_bytes": nbytes,
                         "algorithmic_flops": flops, "GB_s": round(gbs, 1),
                         "TFLOP_s": round(tfs, 1),
                         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
                         "frac_bf16_peak": round(tfs / BF16_PEAK_TFLOPS, 4)}
         del h, t, out, ws
-    del W
+    del W, Wp
     torch.cuda.empty_cache()
     return res
 
@@ -516,11 +526,11 @@ def main():
                     help="skip the token log-probability leg (Qwen3-8B LM head)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-step leg (B = 512, 85 %% decode / 15 %% append rows)")
-    ap.add_argument("--only", choices=["write", "decode", "append", "copy", "mixed"],
+    ap.add_argument("--only", choices=["write", "decode", "append", "copy", "mixed", "logprob"],
                     help="run only this part of the step --steps times after --warmup "
                          "(for rocprofv3 runs; 'copy' is a 1 GiB torch copy used to "
-                         "calibrate the HBM byte counters, 'mixed' the mixed-step leg); "
-                         "prints no JSON line")
+                         "calibrate the HBM byte counters, 'mixed' the mixed-step leg, "
+                         "'logprob' the LM-head log-probability leg); prints no JSON line")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -538,6 +548,10 @@ def main():
     if args.only == "mixed":
         res = mixed_step(ra, synth, dev, args.steps, args.warmup)
         print(f"[bench] mixed step {json.dumps(res)}", flush=True)
+        return
+    if args.only == "logprob":
+        res = logprob_leg(ra, synth, dev, args.steps, args.warmup)
+        print(f"[bench] token_logprob {json.dumps(res)}", flush=True)
         return
     wd, wa = synth.config(2), synth.config(3)
     td, ta = synth.make_tensors(wd, dev), synth.make_tensors(wa, dev)

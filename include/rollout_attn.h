@@ -40,7 +40,7 @@
  *   - Results are deterministic: the same inputs give bitwise the same
  *     outputs, independent of which physical pages the block table names.
  *
- * Paged KV layout (ABI version 2). Page size P = 16 tokens, head dim D = 128.
+ * Paged KV layout (ABI versions 2 and 3). Page size P = 16 tokens, head dim D = 128.
  * Logical token j of row b lives in physical page bt[b * bt_stride + j / P]
  * at slot j % P. Within a page each KV head owns one contiguous block:
  *   K pool  [num_pages][Hkv][P][D]   element (page, g, slot, d) at
@@ -76,7 +76,7 @@
 extern "C" {
 #endif
 
-#define RA_ABI_VERSION 2
+#define RA_ABI_VERSION 3
 #define RA_PAGE_SIZE 16
 #define RA_HEAD_DIM 128
 
@@ -316,6 +316,34 @@ size_t token_logprob_workspace_size(int32_t N, int32_t V);
 int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t N, int32_t V,
                   int32_t D, float scale, float *logprob, float *lse, void *workspace,
                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The same log-probabilities from a packed copy of the LM-head matrix. The
+ * matrix is constant for a policy version, so it can be repacked once into
+ * the order the kernel's matrix products consume it; each wave then streams
+ * one contiguous run of memory instead of 32 rows 128 bytes at a time.
+ * Results are bitwise those of token_logprob on the unpacked matrix.
+ *
+ * Packed layout: bf16, 16-byte units; unit
+ *   i = ((tile * (D / 64) + s) * 4 + u) * 64 + lane
+ * holds W[32 * tile + lane % 32][64 * s + 32 * (lane / 32) + 8 * u + 0..7],
+ * zeros for rows at or past V; tiles cover V rounded up to a multiple of 128.
+ *
+ * token_logprob_packed_weight_size: bytes of the packed copy (0 if V <= 0,
+ *   D <= 0 or D is not a multiple of 64).
+ * token_logprob_pack_weight: writes the packed copy of W (bf16 [V][D]) into
+ *   W_packed (device, packed_bytes >= the size above). Errors: RA_ERR_SHAPE
+ *   (V <= 0, D <= 0), RA_ERR_NULL, RA_ERR_UNSUPPORTED (D % 64 != 0),
+ *   RA_ERR_WORKSPACE (packed_bytes too small), RA_ERR_HIP.
+ * token_logprob_packed: token_logprob with W_packed in place of W; the same
+ *   arguments, errors and workspace size.
+ */
+size_t token_logprob_packed_weight_size(int32_t V, int32_t D);
+int token_logprob_pack_weight(const void *W, int32_t V, int32_t D, void *W_packed,
+                              size_t packed_bytes, hipStream_t stream);
+int token_logprob_packed(const void *h, const void *W_packed, const int32_t *targets, int32_t N,
+                         int32_t V, int32_t D, float scale, float *logprob, float *lse,
+                         void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Page write: scatter new tokens' keys and values into their pages, a bit

@@ -28,7 +28,8 @@ __all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "append_write"
            "kv_page_write",
            "kv_page_gather", "token_logprob", "decode_workspace_size",
            "decode_shared_prefix_workspace_size", "append_workspace_size", "mixed_workspace_size",
-           "token_logprob_workspace_size", "abi_version", "RolloutAttnError"]
+           "token_logprob_workspace_size", "token_logprob_pack_weight", "token_logprob_packed",
+           "abi_version", "RolloutAttnError"]
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -444,22 +445,24 @@ def token_logprob_workspace_size(N: int, V: int) -> int:
     return int(_lib.load().token_logprob_workspace_size(N, V))
 
 
-def token_logprob(h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, scale: float = 1.0,
-                  out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-                  want_lse: bool = False, workspace: Optional[torch.Tensor] = None, stream=None
-                  ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
-    """Log-probability of targets[n] under logits scale * h[n] . W^T.
-
-    h bf16 [N][D], W bf16 [V][D], targets int32 [N] -> logprob fp32 [N] (, lse fp32 [N]).
-    """
+def _token_logprob(h, W, targets, scale, out, lse, want_lse, workspace, stream, packed_V):
+    """Shared marshalling of token_logprob / token_logprob_packed (packed_V: V of a
+    packed matrix, None for a row-major one)."""
     lib = _lib.load()
     dev = h.device
     _need(h, "h", torch.bfloat16, dev)
     _need(W, "W", torch.bfloat16, dev)
     _need(targets, "targets", torch.int32, dev)
     N, D = h.shape
-    V = W.shape[0]
-    _shape(W, (V, D), "W")
+    if packed_V is None:
+        V = W.shape[0]
+        _shape(W, (V, D), "W")
+    else:
+        V = int(packed_V)
+        need = lib.token_logprob_packed_weight_size(V, D)
+        if W.dim() != 1 or W.numel() * 2 < need:
+            raise ValueError(f"W_packed: expected a flat bf16 tensor of {need // 2} elements "
+                             f"for V={V}, D={D}, got {tuple(W.shape)}")
     _shape(targets, (N,), "targets")
     if out is None:
         out = torch.empty((N,), dtype=torch.float32, device=dev)
@@ -474,7 +477,46 @@ def token_logprob(h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, scale
         workspace = torch.empty(max(lib.token_logprob_workspace_size(N, V), 1),
                                 dtype=torch.uint8, device=dev)
     _need(workspace, "workspace", torch.uint8, dev)
-    _lib.check("token_logprob", lib.token_logprob(
+    fn = lib.token_logprob if packed_V is None else lib.token_logprob_packed
+    name = "token_logprob" if packed_V is None else "token_logprob_packed"
+    _lib.check(name, fn(
         h.data_ptr(), W.data_ptr(), targets.data_ptr(), N, V, D, float(scale), out.data_ptr(),
         _ptr(lse), workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
     return out, lse
+
+
+def token_logprob(h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, scale: float = 1.0,
+                  out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                  want_lse: bool = False, workspace: Optional[torch.Tensor] = None, stream=None
+                  ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Log-probability of targets[n] under logits scale * h[n] . W^T.
+
+    h bf16 [N][D], W bf16 [V][D], targets int32 [N] -> logprob fp32 [N] (, lse fp32 [N]).
+    """
+    return _token_logprob(h, W, targets, scale, out, lse, want_lse, workspace, stream, None)
+
+
+def token_logprob_pack_weight(W: torch.Tensor, out: Optional[torch.Tensor] = None,
+                              stream=None) -> torch.Tensor:
+    """Packed copy of the LM-head matrix W bf16 [V][D] for token_logprob_packed
+    (a flat bf16 tensor; rows past V are zeros)."""
+    lib = _lib.load()
+    dev = W.device
+    _need(W, "W", torch.bfloat16, dev)
+    V, D = W.shape
+    n = lib.token_logprob_packed_weight_size(V, D) // 2
+    if out is None:
+        out = torch.empty((max(n, 1),), dtype=torch.bfloat16, device=dev)
+    _need(out, "out", torch.bfloat16, dev)
+    _lib.check("token_logprob_pack_weight", lib.token_logprob_pack_weight(
+        W.data_ptr(), V, D, out.data_ptr(), out.numel() * 2, _stream(dev, stream)))
+    return out
+
+
+def token_logprob_packed(h: torch.Tensor, W_packed: torch.Tensor, V: int, targets: torch.Tensor,
+                         scale: float = 1.0, out: Optional[torch.Tensor] = None,
+                         lse: Optional[torch.Tensor] = None, want_lse: bool = False,
+                         workspace: Optional[torch.Tensor] = None, stream=None
+                         ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """token_logprob with the packed matrix from token_logprob_pack_weight (V rows)."""
+    return _token_logprob(h, W_packed, targets, scale, out, lse, want_lse, workspace, stream, V)

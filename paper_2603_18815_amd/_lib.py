@@ -31,6 +31,9 @@ EXPORTS = (
     "kv_page_gather",
     "token_logprob_workspace_size",
     "token_logprob",
+    "token_logprob_packed_weight_size",
+    "token_logprob_pack_weight",
+    "token_logprob_packed",
 )
 
 
@@ -102,6 +105,12 @@ def load() -> ctypes.CDLL:
     lib.token_logprob_workspace_size.restype = sz
     lib.token_logprob.argtypes = [vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, sz, vp]
     lib.token_logprob.restype = ctypes.c_int
+    lib.token_logprob_packed_weight_size.argtypes = [i32, i32]
+    lib.token_logprob_packed_weight_size.restype = sz
+    lib.token_logprob_pack_weight.argtypes = [vp, i32, i32, vp, sz, vp]
+    lib.token_logprob_pack_weight.restype = ctypes.c_int
+    lib.token_logprob_packed.argtypes = [vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, sz, vp]
+    lib.token_logprob_packed.restype = ctypes.c_int
     lib.kv_page_write.argtypes = [vp, vp, vp, vp, kvp, i32, i32, i32, i32, vp]
     lib.kv_page_write.restype = ctypes.c_int
     lib.kv_page_gather.argtypes = [kvp, vp, vp, i32, i32, i32, vp, vp, vp]

@@ -271,7 +271,36 @@ int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t 
   if (!workspace || workspace_bytes < ra::logprob_workspace_bytes(N, V)) return RA_ERR_WORKSPACE;
   return hip_status(ra::launch_logprob(static_cast<const uint16_t *>(h),
                                        static_cast<const uint16_t *>(W), targets, N, V, D, scale,
-                                       logprob, lse, workspace, stream));
+                                       logprob, lse, workspace, false, stream));
+}
+
+size_t token_logprob_packed_weight_size(int32_t V, int32_t D) {
+  if (V <= 0 || D <= 0 || D % 64 != 0) return 0;
+  return ra::logprob_packed_bytes(V, D);
+}
+
+int token_logprob_pack_weight(const void *W, int32_t V, int32_t D, void *W_packed,
+                              size_t packed_bytes, hipStream_t stream) {
+  if (V <= 0 || D <= 0) return RA_ERR_SHAPE;
+  if (!W || !W_packed) return RA_ERR_NULL;
+  if (D % 64 != 0) return RA_ERR_UNSUPPORTED;
+  if (packed_bytes < ra::logprob_packed_bytes(V, D)) return RA_ERR_WORKSPACE;
+  return hip_status(ra::launch_logprob_pack(static_cast<const uint16_t *>(W), V, D,
+                                            static_cast<uint16_t *>(W_packed), stream));
+}
+
+int token_logprob_packed(const void *h, const void *W_packed, const int32_t *targets, int32_t N,
+                         int32_t V, int32_t D, float scale, float *logprob, float *lse,
+                         void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (N < 0 || V <= 0 || D <= 0) return RA_ERR_SHAPE;
+  if (!h || !W_packed || !targets || !logprob) return RA_ERR_NULL;
+  if (D % 64 != 0) return RA_ERR_UNSUPPORTED;
+  if (N == 0) return RA_OK;
+  if (ra::logprob_grid(N, V) > 0x7fffffff) return RA_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < ra::logprob_workspace_bytes(N, V)) return RA_ERR_WORKSPACE;
+  return hip_status(ra::launch_logprob(static_cast<const uint16_t *>(h),
+                                       static_cast<const uint16_t *>(W_packed), targets, N, V, D,
+                                       scale, logprob, lse, workspace, true, stream));
 }
 
 int kv_page_write(const void *k_new, const void *v_new, const int32_t *cu_new,

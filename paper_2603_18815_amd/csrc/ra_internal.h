@@ -84,7 +84,10 @@ size_t logprob_workspace_bytes(int32_t N, int32_t V);
 int64_t logprob_grid(int32_t N, int32_t V);
 hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *targets, int32_t N,
                           int32_t V, int32_t D, float scale, float *logp, float *lse,
-                          void *workspace, hipStream_t stream);
+                          void *workspace, bool packed, hipStream_t stream);
+size_t logprob_packed_bytes(int32_t V, int32_t D);
+hipError_t launch_logprob_pack(const uint16_t *W, int32_t V, int32_t D, uint16_t *Wp,
+                               hipStream_t stream);
 
 // ---- page write / gather ----
 hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,

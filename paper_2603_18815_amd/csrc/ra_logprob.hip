@@ -25,6 +25,13 @@
 //
 // Combine kernel: one wave per token merges its partials in chunk order:
 // M = max_c m_c, L = sum_c l_c 2^(m_c - M), lse = (M + log2 L) ln 2.
+//
+// Packed LM head: W [V][D] row-major makes every wave read 32 rows 128 bytes
+// at a time, 8 KB apart. The packed copy stores each 32-row tile in the order
+// the products consume it, [V/32][D/64][4][64 lanes][8], so a wave's whole
+// stream over D is one contiguous run and each load instruction reads 1 KB
+// contiguous. Same products in the same order: the results are bitwise those
+// of the row-major matrix.
 #include "ra_device.h"
 #include "ra_internal.h"
 
@@ -70,7 +77,7 @@ __device__ __forceinline__ float pair_sum(float x) {
 }
 
 // kTiles 32-token tiles per workgroup: 2 for small batches (N <= 64), else 4.
-template <int kTiles>
+template <int kTiles, bool kPacked>
 __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobArgs a) {
   constexpr int kTokenBlock = 32 * kTiles;
   // XCD-aware placement: workgroup ids are dealt to the XCDs round-robin, so
@@ -88,9 +95,12 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   const int v0 = chunk * kVocabChunk + wave * 32;       // first vocabulary row of this wave
   const int t0 = tblock * kTokenBlock;                  // first token of the block
 
-  // A row (vocabulary) this lane supplies, clamped into range for the loads;
-  // rows past V are masked after the products.
-  const uint16_t *wp = a.W + (size_t)min(v0 + col, a.V - 1) * a.D + 32 * half;
+  // A row (vocabulary) this lane supplies, clamped into range for the loads
+  // (packed: rows past V are stored as zeros); rows past V are masked after
+  // the products.
+  const uint16_t *wp =
+      kPacked ? a.W + (size_t)(v0 / 32) * 32 * a.D + 8 * lane
+              : a.W + (size_t)min(v0 + col, a.V - 1) * a.D + 32 * half;
   // h staging: thread i copies 16-byte chunks i + 256 j (j = 0..3) of the
   // block's 128 x 64 slice (token = chunk / 8, 8 dims per chunk); tokens past
   // N are clamped (their columns are never written back).
@@ -119,7 +129,8 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   bf16x8 w0[4], w1[4], w2[4], w3[4];
   auto w_load = [&](bf16x8 *dst, int s) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) dst[u] = load_bf16x8(wp + s * kDimStep + 8 * u);
+    for (int u = 0; u < 4; ++u)
+      dst[u] = load_bf16x8(kPacked ? wp + (size_t)(4 * s + u) * 8 * kWave : wp + s * kDimStep + 8 * u);
   };
   const int nsteps = a.D / kDimStep;
   const int last = nsteps - 1;
@@ -213,6 +224,25 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   }
 }
 
+// Packed copy of W: 16-byte unit i = ((tile * D/64 + s) * 4 + u) * 64 + lane
+// holds W[32 tile + lane % 32][64 s + 32 (lane / 32) + 8 u + 0..7] (zeros for
+// rows past V).
+__global__ __launch_bounds__(256) void logprob_pack_kernel(const uint16_t *__restrict__ W,
+                                                           int32_t V, int32_t D, size_t units,
+                                                           uint16_t *__restrict__ Wp) {
+  const size_t steps = (size_t)(D / kDimStep);
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < units;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const int lane = (int)(i % kWave), u = (int)((i / kWave) % 4);
+    const size_t s = (i / (4 * kWave)) % steps, tile = i / (4 * kWave * steps);
+    const size_t row = 32 * tile + (lane & 31);
+    const size_t dim = kDimStep * s + 32 * (lane >> 5) + 8 * u;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < (size_t)V) v = load_u32x4(W + row * D + dim);
+    store_u32x4(Wp + 8 * i, v);
+  }
+}
+
 __global__ __launch_bounds__(kLpThreads) void logprob_combine_kernel(LogprobArgs a, float *logp,
                                                                    float *lse) {
   const int lane = threadIdx.x & (kWave - 1);
@@ -242,6 +272,21 @@ __global__ __launch_bounds__(kLpThreads) void logprob_combine_kernel(LogprobArgs
 
 int32_t logprob_chunks(int32_t V) { return (V + kVocabChunk - 1) / kVocabChunk; }
 
+// The packed copy covers every row a workgroup reads: V rounded up to whole
+// 128-row chunks.
+size_t logprob_packed_bytes(int32_t V, int32_t D) {
+  return (size_t)logprob_chunks(V) * kVocabChunk * D * sizeof(uint16_t);
+}
+
+hipError_t launch_logprob_pack(const uint16_t *W, int32_t V, int32_t D, uint16_t *Wp,
+                               hipStream_t stream) {
+  const size_t units = logprob_packed_bytes(V, D) / 16;
+  const size_t want = (units + 255) / 256, blocks = want < 65536 ? want : 65536;
+  hipLaunchKernelGGL(logprob_pack_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, W, V, D,
+                     units, Wp);
+  return hipGetLastError();
+}
+
 size_t logprob_workspace_bytes(int32_t N, int32_t V) {
   return ((size_t)N * logprob_chunks(V) * 2 + (size_t)N) * sizeof(float);
 }
@@ -258,7 +303,7 @@ int64_t logprob_grid(int32_t N, int32_t V) {
 
 hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *targets, int32_t N,
                           int32_t V, int32_t D, float scale, float *logp, float *lse,
-                          void *workspace, hipStream_t stream) {
+                          void *workspace, bool packed, hipStream_t stream) {
   LogprobArgs a;
   a.h = h;
   a.W = W;
@@ -275,10 +320,16 @@ hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *t
   a.scale = scale;
   a.scale_log2 = scale * kLog2e;
   const dim3 grid((unsigned)logprob_grid(N, V));
-  if (tiles == 2)
-    hipLaunchKernelGGL(logprob_partial_kernel<2>, grid, dim3(kLpThreads), 0, stream, a);
+  if (tiles == 2 && packed)
+    hipLaunchKernelGGL((logprob_partial_kernel<2, true>), grid, dim3(kLpThreads), 0, stream, a);
+  else if (tiles == 2)
+    hipLaunchKernelGGL((logprob_partial_kernel<2, false>), grid, dim3(kLpThreads), 0, stream, a);
+  else if (packed)
+    hipLaunchKernelGGL((logprob_partial_kernel<kMaxTiles, true>), grid, dim3(kLpThreads), 0,
+                       stream, a);
   else
-    hipLaunchKernelGGL(logprob_partial_kernel<kMaxTiles>, grid, dim3(kLpThreads), 0, stream, a);
+    hipLaunchKernelGGL((logprob_partial_kernel<kMaxTiles, false>), grid, dim3(kLpThreads), 0,
+                       stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(logprob_combine_kernel, dim3((N + kLpWaves - 1) / kLpWaves),

@@ -42,7 +42,7 @@ def test_exports_every_declared_symbol(lib):
 
 def test_abi_version_and_status_strings(lib):
     declared = int(re.search(r"#define RA_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
-    assert lib.ra_abi_version() == declared == 2
+    assert lib.ra_abi_version() == declared == 3
     assert lib.ra_status_string(0) == b"RA_OK"
     assert lib.ra_status_string(4) == b"RA_ERR_WORKSPACE"
     assert lib.ra_status_string(99) == b"RA_UNKNOWN_STATUS"
@@ -128,6 +128,37 @@ def test_token_logprob_validation(lib):
     f = lib.token_logprob_workspace_size
     assert f(0, 100) == 0 and f(8, 0) == 0
     assert f(64, 151936) == (64 * 1187 * 2 + 64) * 4     # 1187 chunks of 128 rows
+
+
+def test_token_logprob_packed_validation(lib):
+    size = lib.token_logprob_packed_weight_size
+    assert size(151936, 4096) == 1187 * 128 * 4096 * 2   # V rounded up to 128-row chunks
+    assert size(1, 64) == 128 * 64 * 2
+    assert size(0, 64) == 0 and size(10, 0) == 0 and size(10, 96) == 0
+
+    def pack(**kw):
+        d = dict(W=FAKE, V=100, D=128, Wp=FAKE, nbytes=1 << 30)
+        d.update(kw)
+        return lib.token_logprob_pack_weight(d["W"], d["V"], d["D"], d["Wp"], d["nbytes"], None)
+    assert pack(W=None) == _lib.RA_ERR_NULL
+    assert pack(Wp=None) == _lib.RA_ERR_NULL
+    assert pack(V=0) == _lib.RA_ERR_SHAPE
+    assert pack(D=-64) == _lib.RA_ERR_SHAPE
+    assert pack(D=96) == _lib.RA_ERR_UNSUPPORTED
+    assert pack(nbytes=128 * 128 * 2 - 1) == _lib.RA_ERR_WORKSPACE
+
+    def call(**kw):
+        d = dict(h=FAKE, W=FAKE, t=FAKE, N=8, V=100, D=128, out=FAKE, ws=FAKE, ws_bytes=1 << 30)
+        d.update(kw)
+        return lib.token_logprob_packed(d["h"], d["W"], d["t"], d["N"], d["V"], d["D"], 1.0,
+                                        d["out"], None, d["ws"], d["ws_bytes"], None)
+    assert call(W=None) == _lib.RA_ERR_NULL
+    assert call(t=None) == _lib.RA_ERR_NULL
+    assert call(N=-1) == _lib.RA_ERR_SHAPE
+    assert call(V=0) == _lib.RA_ERR_SHAPE
+    assert call(D=96) == _lib.RA_ERR_UNSUPPORTED
+    assert call(ws_bytes=4) == _lib.RA_ERR_WORKSPACE
+    assert call(N=0) == _lib.RA_OK
 
 
 def test_append_validation(lib):

@@ -104,3 +104,74 @@ def test_token_logprob_qwen3_lm_head(device):
     torch.cuda.synchronize()
     ref_lp, ref_ls = oracle.token_logprob(bits(h), bits(W), t.cpu().numpy(), 1.0)
     check(lp, ls, ref_lp, ref_ls, "Qwen3-8B LM head, 64 tokens")
+
+
+def packed_layout(W_bits, V, D):
+    """The packed LM-head layout restated from its definition: 16-byte unit
+    ((tile * D/64 + s) * 4 + u) * 64 + lane holds row 32 tile + lane % 32,
+    dims 64 s + 32 (lane / 32) + 8 u + 0..7; rows past V (up to a multiple of
+    128) are zeros."""
+    Vp = (V + 127) // 128 * 128
+    Wz = np.zeros((Vp, D), np.uint16)
+    Wz[:V] = W_bits
+    x = Wz.reshape(Vp // 32, 32, D // 64, 2, 4, 8)      # tile, row, s, half, u, e
+    x = x.transpose(0, 2, 4, 3, 1, 5)                   # tile, s, u, half, row, e
+    return x.reshape(-1)                                # lane = 32 half + row
+
+
+@pytest.mark.parametrize("V,D", [(200, 128), (128, 64), (1, 192), (1000, 256)])
+def test_pack_weight_layout(device, V, D):
+    """The packed copy is bit-exactly the documented permutation of W."""
+    say(f"token_logprob_pack_weight V={V} D={D}")
+    _, W = inputs(V + D, 1, V, D, device)
+    Wp = ra.token_logprob_pack_weight(W)
+    torch.cuda.synchronize()
+    assert Wp.numel() == (V + 127) // 128 * 128 * D
+    assert np.array_equal(bits(Wp), packed_layout(bits(W), V, D))
+
+
+@pytest.mark.parametrize("N,V,D,scale", [
+    (70, 1000, 128, 1.0),
+    (5, 257, 192, 0.7),
+    (1, 1, 64, 1.0),
+    (130, 4096, 256, 1.0),
+    (64, 3001, 320, 1.3),
+])
+def test_token_logprob_packed_matches(device, N, V, D, scale):
+    """token_logprob_packed gives bitwise the row-major results, and both meet
+    the oracle."""
+    say(f"token_logprob_packed N={N} V={V} D={D} scale={scale}")
+    h, W = inputs(N + V + D + 1, N, V, D, device)
+    rng = np.random.default_rng(N + V + 1)
+    t = rng.integers(0, V, size=N).astype(np.int32)
+    if N >= 5:
+        t[:4] = [0, V - 1, -1, V]
+    tt = torch.as_tensor(t, device=device)
+    Wp = ra.token_logprob_pack_weight(W)
+    lp, ls = ra.token_logprob(h, W, tt, scale, want_lse=True)
+    lp2, ls2 = ra.token_logprob_packed(h, Wp, V, tt, scale, want_lse=True)
+    torch.cuda.synchronize()
+    assert torch.equal(lp.isnan(), lp2.isnan())
+    assert torch.equal(torch.nan_to_num(lp), torch.nan_to_num(lp2)) and torch.equal(ls, ls2)
+    ref_lp, ref_ls = oracle.token_logprob(bits(h), bits(W), t, scale)
+    check(lp2, ls2, ref_lp, ref_ls, f"packed N={N} V={V} D={D}")
+
+
+@pytest.mark.parametrize("N", [64, 1024])
+def test_token_logprob_packed_qwen3_lm_head(device, N):
+    """The Qwen3-8B LM head at the benchmark's batch sizes: packed and row-major
+    bitwise equal; 16 sampled tokens against the oracle."""
+    V, D = 151936, 4096
+    say(f"token_logprob_packed Qwen3-8B LM head N={N}")
+    h, W = inputs(80 + N, N, V, D, device)
+    t = torch.randint(0, V, (N,), dtype=torch.int32, device=device,
+                      generator=synth.value_generator(80 + N, device))
+    Wp = ra.token_logprob_pack_weight(W)
+    lp, ls = ra.token_logprob(h, W, t, 1.0, want_lse=True)
+    lp2, ls2 = ra.token_logprob_packed(h, Wp, V, t, 1.0, want_lse=True)
+    torch.cuda.synchronize()
+    assert torch.equal(lp, lp2) and torch.equal(ls, ls2)
+    del Wp
+    pick = np.random.default_rng(N).choice(N, size=16, replace=False)
+    ref_lp, ref_ls = oracle.token_logprob(bits(h)[pick], bits(W), t.cpu().numpy()[pick], 1.0)
+    check(lp2[pick], ls2[pick], ref_lp, ref_ls, f"packed Qwen3-8B LM head, N={N} (16 sampled)")
