@@ -229,7 +229,11 @@ def quantize(x_bits, scale):
     x = _u16(x_bits)
     f = (x.astype(np.uint32) << 16).view(np.float32)
     inv = np.float32(1.0) / np.float32(scale)
-    return e4m3_encode((f * inv).astype(np.float32))
+    # inf / NaN inputs and fp32 overflow are meant (IEEE results; the encoder
+    # saturates infinities and maps NaN to its NaN code)
+    with np.errstate(over="ignore", invalid="ignore"):
+        y = (f * inv).astype(np.float32)
+    return e4m3_encode(y)
 
 
 def page_write_fp8(k_new, v_new, cu_new, start_pos, block_table, k_pool, v_pool, k_scale,
