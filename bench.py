@@ -111,6 +111,14 @@ def cpu_baseline(wd, td, wa, ta, seconds: float):
     from synth import bits, compact_rows
 
     cores = oracle.num_threads()
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     # decode: whole rows of the decode workload, taken in a fixed order until the budget
     rng = np.random.default_rng(0)
     order = rng.permutation(wd.kv_lens.shape[0])
@@ -130,6 +138,7 @@ def cpu_baseline(wd, td, wa, ta, seconds: float):
         if spent > seconds:
             break
     dec = {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
+           "cpu_model": cpu_model,
            "sample": f"decode, {rows_done} of {wd.kv_lens.shape[0]} rows of the decode "
                      f"workload (all heads), {spent:.1f} s wall"}
     # append: single queries (query i of a row == a one-token chunk at ctx + i),
@@ -152,6 +161,7 @@ def cpu_baseline(wd, td, wa, ta, seconds: float):
         flops += 4 * 128 * wa.Hq * int((ctx1.astype(np.int64) + 1).sum())
         nq += len(qs)
     app = {"value": flops / spent_a / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+           "cpu_model": cpu_model,
            "sample": f"append, {nq} single queries (all heads) drawn from random rows of the "
                      f"append workload, {spent_a:.1f} s wall"}
     return dec, app
@@ -683,10 +693,12 @@ def main():
             "new_tokens_written": n_new,
             "parallelism": "1 GPU",
         },
-        "decode": {"ms": round(float(d_ms.mean()), 4), "ms_min": round(float(d_ms.min()), 4),
+        "decode": {"ms": round(float(d_ms.mean()), 4), "ms_median": round(float(np.median(d_ms)), 4),
+                   "ms_min": round(float(d_ms.min()), 4),
                    "algorithmic_bytes": dbytes, "GB_s": round(dec_gbs, 1),
                    "frac_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
-        "append": {"ms": round(float(a_ms.mean()), 4), "ms_min": round(float(a_ms.min()), 4),
+        "append": {"ms": round(float(a_ms.mean()), 4), "ms_median": round(float(np.median(a_ms)), 4),
+                   "ms_min": round(float(a_ms.min()), 4),
                    "algorithmic_flops": aflops, "TFLOP_s": round(app_tfs, 1),
                    "frac_bf16_peak": round(app_tfs / BF16_PEAK_TFLOPS, 4)},
         "page_write": {"ms": round(float(w_ms.mean()), 4), "algorithmic_bytes": wbytes,
