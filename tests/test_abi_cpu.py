@@ -296,3 +296,24 @@ def test_append_write_validation(lib):
         _lib.RA_ERR_UNSUPPORTED
     assert call(_kv(), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
     assert call(_kv(), total_q=0, ws=None) == _lib.RA_OK
+
+
+def test_plain_c_caller(tmp_path):
+    """The header is valid C99 on its own and a C program links the library:
+    tests/c_abi_check.c calls every entry point (host-side rejections only)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    rocm_inc = "/opt/rocm/include"
+    if gcc is None or not os.path.isdir(rocm_inc):
+        pytest.skip("gcc or the ROCm headers are not available")
+    libdir = os.path.dirname(_lib.LIB_PATH)
+    exe = tmp_path / "c_abi_check"
+    cmd = [gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(ROOT, "include"), "-I", rocm_inc,
+           os.path.join(ROOT, "tests", "c_abi_check.c"), "-L", libdir, "-lrollout_attn",
+           f"-Wl,-rpath,{libdir}", "-o", str(exe)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok (0 failed)"), r.stdout + r.stderr
