@@ -1,5 +1,6 @@
 // Append attention tile (causal chunked prefill against the paged cache),
-// shared by the append kernel and the mixed decode + append kernel.
+// run by the planned persistent kernel for append calls and for mixed
+// decode + append calls.
 //
 // One workgroup (8 waves, two per SIMD) owns a block of QB = 256 / G
 // consecutive queries of one row and all G query heads of one KV head: 256
