@@ -58,11 +58,11 @@
  *                   value x is stored as encode(fp32(x) * fp32(1 / scale)):
  *                   round to nearest even, magnitudes beyond 448 (and
  *                   infinities) saturate to +-448, NaN becomes 0x7F.
- *   fp8 pools are supported by every entry point except
- *   rollout_attn_append_write (RA_ERR_UNSUPPORTED); kv_page_write quantizes,
- *   kv_page_gather copies the codes out, the attention entry points convert
- *   the codes exactly to bf16 operands. A mixed call takes one element type
- *   for both sides (RA_ERR_UNSUPPORTED otherwise).
+ *   fp8 pools are supported by every entry point: kv_page_write (and the
+ *   write of rollout_attn_append_write) quantizes, kv_page_gather copies the
+ *   codes out, the attention entry points convert the codes exactly to bf16
+ *   operands. A mixed call takes one element type for both sides
+ *   (RA_ERR_UNSUPPORTED otherwise).
  */
 #ifndef ROLLOUT_ATTN_H
 #define ROLLOUT_ATTN_H
@@ -86,7 +86,7 @@ typedef enum {
   RA_ERR_SHAPE = 2,       /* inconsistent sizes (negative, Hq % Hkv != 0, ...) */
   RA_ERR_UNSUPPORTED = 3, /* valid but not built: page_size != 16, head_dim != 128,
                              decode group size Hq / Hkv > 16, an unknown kv_dtype,
-                             an fp8 pool where it is not supported */
+                             pools of two element types in one mixed call */
   RA_ERR_WORKSPACE = 4,   /* workspace smaller than the *_workspace_size value */
   RA_ERR_HIP = 5          /* a HIP launch failed (no device, bad stream, ...) */
 } ra_status;
@@ -235,9 +235,11 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
  *   k_new, v_new  bf16 [total_q][Hkv][128]: the chunk tokens' keys and values,
  *                 packed like q; token i of row b goes to position
  *                 ctx_lens[b] + i
+ * fp8 pools: the chunk is quantized as by kv_page_write (encode(fp32(x) *
+ * fp32(1 / scale)), see the layout above) and attended as stored.
  * Precondition (not checked): no row of the call reads, below its ctx, a page
  * slot that another row of the call writes.
- * Errors: as rollout_attn_append; RA_ERR_UNSUPPORTED for fp8 pools.
+ * Errors: as rollout_attn_append.
  */
 int rollout_attn_append_write(const void *q, const void *k_new, const void *v_new,
                               const int32_t *cu_q, const int32_t *ctx_lens, const ra_paged_kv *kv,

@@ -167,7 +167,6 @@ int rollout_attn_append_write(const void *q, const void *k_new, const void *v_ne
   int s = check_kv(kv);
   if (s != RA_OK) return s;
   if (!q || !k_new || !v_new || !cu_q || !ctx_lens || !out) return RA_ERR_NULL;
-  if (is_fp8(kv)) return RA_ERR_UNSUPPORTED;
   if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
   if (Hq / kv->num_kv_heads > 256 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
   if (!positions_fit(kv, max_kv_len) || max_q_len > max_kv_len) return RA_ERR_SHAPE;

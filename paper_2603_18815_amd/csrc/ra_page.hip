@@ -3,8 +3,9 @@
 // One workgroup moves one (row, page, KV head) block per pool; V goes through
 // LDS so that both sides are accessed in 8- or 16-byte pieces per lane.
 // bf16 pools: bit copies. fp8 pools: the write quantizes each bf16 element to
-// its E4M3 code (x * fp32(1 / scale), round to nearest even, saturated), the
-// gather copies the codes out.
+// its E4M3 code (x * fp32(1 / scale), round to nearest even, saturated; the
+// block code is shared with the fused append launch), the gather copies the
+// codes out.
 #include "ra_device.h"
 #include "ra_internal.h"
 #include "ra_page_write.h"
@@ -15,14 +16,15 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kVPitch = kHeadDim + 8;  // LDS row pitch (elements) of the staged V slots
 
-// bf16 pools: one (row, page, KV head) block per workgroup.
+// One (row, page, KV head) block per workgroup.
+template <bool kFp8>
 __global__ __launch_bounds__(pwrite::kItemThreads) void page_write_kernel(pwrite::WriteArgs a) {
   const pwrite::WriteItem it = pwrite::write_item(a, blockIdx.x, blockIdx.z);
   if (!it.active) return;
   __shared__ uint16_t sv[kPage][pwrite::kVPitch];
-  pwrite::write_phase1(a, it, blockIdx.y, threadIdx.x, sv);
+  pwrite::write_phase1<kFp8>(a, it, blockIdx.y, threadIdx.x, sv);
   __syncthreads();
-  pwrite::write_phase2(a, it, blockIdx.y, threadIdx.x, sv);
+  pwrite::write_phase2<kFp8>(a, it, blockIdx.y, threadIdx.x, sv);
 }
 
 __global__ __launch_bounds__(kThreads) void page_gather_kernel(
@@ -55,53 +57,6 @@ __global__ __launch_bounds__(kThreads) void page_gather_kernel(
     const size_t src = (((size_t)id * hkv + g) * kPage + slot) * kHeadDim + ch * 8;
     store_u32x4(k_out + dst, load_u32x4(k_pool + src));
     store_u32x4(v_out + dst, *reinterpret_cast<const u32x4 *>(&sv[slot][ch * 8]));
-  }
-}
-
-// fp8 pools: one byte per element; a lane quantizes 8 elements (16 bytes of
-// bf16 in, 8 bytes of codes out).
-__global__ __launch_bounds__(kThreads) void page_write_fp8_kernel(
-    const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
-    const int32_t *__restrict__ cu_new, const int32_t *__restrict__ start_pos,
-    uint8_t *__restrict__ k_pool, uint8_t *__restrict__ v_pool,
-    const int32_t *__restrict__ block_table, int bt_stride, int num_pages, int hkv,
-    int total_new, int max_new, int max_pos, float k_inv, float v_inv) {
-  const int chunk = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x;
-  const int cu0 = min(max(cu_new[b], 0), total_new);
-  const int n = min(min(max(cu_new[b + 1] - cu0, 0), max_new), total_new - cu0);
-  if (n <= 0) return;
-  const int s = min(max(start_pos[b], 0), max_pos - n);
-  if (s < 0) return;
-  const int pg = s / kPage + chunk;
-  if (pg > (s + n - 1) / kPage) return;
-  const int lo = max(s, pg * kPage), hi = min(s + n, pg * kPage + kPage);
-  const int id = clamp_page(block_table[(size_t)b * bt_stride + pg], num_pages);
-
-  __shared__ uint16_t sv[kPage][kVPitch];
-  const int slot = tid >> 4, ch = tid & 15;
-  const int pos = pg * kPage + slot;
-  if (pos >= lo && pos < hi) {
-    const size_t src = ((size_t)(cu0 + pos - s) * hkv + g) * kHeadDim + ch * 8;
-    const size_t dst = (((size_t)id * hkv + g) * kPage + slot) * kHeadDim + ch * 8;
-    *reinterpret_cast<u32x2 *>(k_pool + dst) = quantize8(load_u32x4(k_new + src), k_inv);
-    *reinterpret_cast<u32x4 *>(&sv[slot][ch * 8]) = load_u32x4(v_new + src);
-  }
-  __syncthreads();
-  const int d = tid >> 1, s0 = (tid & 1) * 8;
-  uint8_t *dst = v_pool + (((size_t)id * hkv + g) * kHeadDim + d) * kPage + s0;
-  const int p0 = pg * kPage + s0;
-  u32x4 t;
-#pragma unroll
-  for (int e = 0; e < 4; ++e)
-    t[e] = (uint32_t)sv[s0 + 2 * e][d] | ((uint32_t)sv[s0 + 2 * e + 1][d] << 16);
-  const u32x2 q = quantize8(t, v_inv);
-  if (p0 >= lo && p0 + 8 <= hi) {
-    *reinterpret_cast<u32x2 *>(dst) = q;
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (p0 + e >= lo && p0 + e < hi) dst[e] = (uint8_t)(q[e >> 2] >> (8 * (e & 3)));
   }
 }
 
@@ -144,17 +99,12 @@ hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const
                              hipStream_t stream) {
   // A run of n tokens touches at most (n - 1) / 16 + 2 pages.
   const dim3 grid((max_new + kPage - 1) / kPage + 1, kv.hkv, B);
+  const pwrite::WriteArgs a = pwrite::write_args(k_new, v_new, cu_new, start_pos, kv, total_new,
+                                                 max_new, max_pos);
   if (kv.fp8)
-    hipLaunchKernelGGL(page_write_fp8_kernel, grid, dim3(kThreads), 0, stream, k_new, v_new,
-                       cu_new, start_pos, reinterpret_cast<uint8_t *>(kv.k_pool),
-                       reinterpret_cast<uint8_t *>(kv.v_pool), kv.block_table, kv.bt_stride,
-                       kv.num_pages, kv.hkv, total_new, max_new, max_pos, 1.0f / kv.k_scale,
-                       1.0f / kv.v_scale);
+    hipLaunchKernelGGL(page_write_kernel<true>, grid, dim3(pwrite::kItemThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(page_write_kernel, grid, dim3(pwrite::kItemThreads), 0, stream,
-                       pwrite::WriteArgs{k_new, v_new, cu_new, start_pos, kv.k_pool, kv.v_pool,
-                                         kv.block_table, kv.bt_stride, kv.num_pages, kv.hkv,
-                                         total_new, max_new, max_pos});
+    hipLaunchKernelGGL(page_write_kernel<false>, grid, dim3(pwrite::kItemThreads), 0, stream, a);
   return hipGetLastError();
 }
 

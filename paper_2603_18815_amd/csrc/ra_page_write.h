@@ -1,12 +1,15 @@
-// Page write of one (row, page, KV head) block of bf16 K/V, shared by the
-// page write kernel and the planned append launch that writes the chunks
-// itself. 256 threads move one block: K rows are copied 16 bytes per lane
-// into the token-major page; V tokens go through LDS so that the dim-major
-// page is written 16 bytes per lane as well (partial pages: 2-byte stores on
-// the touched slots only).
+// Page write of one (row, page, KV head) block of K/V, shared by the page
+// write kernel and the planned append launch that writes the chunks itself.
+// 256 threads move one block: K rows go to the token-major page 16 source
+// bytes per lane; V tokens go through LDS so that the dim-major page is
+// written in 8- or 16-byte pieces per lane as well (partial pages: element
+// stores on the touched slots only).
+// bf16 pools: bit copies. fp8 pools (kFp8): each bf16 element is stored as
+// its E4M3 code of x * fp32(1 / scale) (round to nearest even, saturated).
 #pragma once
 
 #include "ra_device.h"
+#include "ra_internal.h"
 
 namespace ra {
 namespace pwrite {
@@ -17,10 +20,37 @@ constexpr int kVPitch = kHeadDim + 8;   // LDS row pitch (elements) of the stage
 struct WriteArgs {
   const uint16_t *k_new, *v_new;       // bf16 [total_new][Hkv][128]
   const int32_t *cu_new, *start_pos;
-  uint16_t *k_pool, *v_pool;
+  uint16_t *k_pool, *v_pool;           // bf16 elements, or E4M3 bytes (fp8 pools)
   const int32_t *block_table;
   int32_t bt_stride, num_pages, hkv, total_new, max_new, max_pos;
+  bool fp8;                            // the pools hold E4M3 codes
+  float k_inv, v_inv;                  // fp8 pools: fp32(1 / k_scale), fp32(1 / v_scale)
 };
+
+// Write arguments for pool kv (the reciprocal scales are taken in fp32, as
+// the quantization rule states).
+inline WriteArgs write_args(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
+                            const int32_t *start_pos, const PagedKV &kv, int32_t total_new,
+                            int32_t max_new, int32_t max_pos) {
+  WriteArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.cu_new = cu_new;
+  a.start_pos = start_pos;
+  a.k_pool = kv.k_pool;
+  a.v_pool = kv.v_pool;
+  a.block_table = kv.block_table;
+  a.bt_stride = kv.bt_stride;
+  a.num_pages = kv.num_pages;
+  a.hkv = kv.hkv;
+  a.total_new = total_new;
+  a.max_new = max_new;
+  a.max_pos = max_pos;
+  a.fp8 = kv.fp8;
+  a.k_inv = kv.fp8 ? 1.0f / kv.k_scale : 1.f;
+  a.v_inv = kv.fp8 ? 1.0f / kv.v_scale : 1.f;
+  return a;
+}
 
 // The block: row b's page s / 16 + chunk (row-relative), KV head g; tokens
 // [lo, hi) of that page are written (positions), cu0 + (pos - s) the source.
@@ -48,35 +78,55 @@ __device__ __forceinline__ WriteItem write_item(const WriteArgs &a, int chunk, i
 }
 
 // Phase 1 (thread t of 256): K rows to the page, V tokens into LDS.
+template <bool kFp8>
 __device__ __forceinline__ void write_phase1(const WriteArgs &a, const WriteItem &it, int g,
                                              int t, uint16_t (*sv)[kVPitch]) {
-  const int slot = t >> 4, ch = t & 15;            // token slot, 16-byte chunk
+  const int slot = t >> 4, ch = t & 15;            // token slot, 8-element chunk
   const int pos = it.pg * kPage + slot;
   if (pos >= it.lo && pos < it.hi) {
     const size_t src = ((size_t)(it.cu0 + pos - it.s) * a.hkv + g) * kHeadDim + ch * 8;
     const size_t dst = (((size_t)it.id * a.hkv + g) * kPage + slot) * kHeadDim + ch * 8;
-    store_u32x4(a.k_pool + dst, load_u32x4(a.k_new + src));
+    if constexpr (kFp8)
+      *reinterpret_cast<u32x2 *>(reinterpret_cast<uint8_t *>(a.k_pool) + dst) =
+          quantize8(load_u32x4(a.k_new + src), a.k_inv);
+    else
+      store_u32x4(a.k_pool + dst, load_u32x4(a.k_new + src));
     *reinterpret_cast<u32x4 *>(&sv[slot][ch * 8]) = load_u32x4(a.v_new + src);
   }
 }
 
 // Phase 2 (after a barrier): the V page is [d][slot]; thread t -> one d row,
 // eight slots.
+template <bool kFp8>
 __device__ __forceinline__ void write_phase2(const WriteArgs &a, const WriteItem &it, int g,
                                              int t, const uint16_t (*sv)[kVPitch]) {
   const int d = t >> 1, s0 = (t & 1) * 8;
-  uint16_t *dst = a.v_pool + (((size_t)it.id * a.hkv + g) * kHeadDim + d) * kPage + s0;
+  const size_t off = (((size_t)it.id * a.hkv + g) * kHeadDim + d) * kPage + s0;
   const int p0 = it.pg * kPage + s0;
-  if (p0 >= it.lo && p0 + 8 <= it.hi) {
-    u32x4 w;
+  u32x4 w;
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      w[e] = (uint32_t)sv[s0 + 2 * e][d] | ((uint32_t)sv[s0 + 2 * e + 1][d] << 16);
-    store_u32x4(dst, w);
+  for (int e = 0; e < 4; ++e)
+    w[e] = (uint32_t)sv[s0 + 2 * e][d] | ((uint32_t)sv[s0 + 2 * e + 1][d] << 16);
+  const bool whole = p0 >= it.lo && p0 + 8 <= it.hi;
+  if constexpr (kFp8) {
+    uint8_t *dst = reinterpret_cast<uint8_t *>(a.v_pool) + off;
+    const u32x2 q = quantize8(w, a.v_inv);
+    if (whole) {
+      *reinterpret_cast<u32x2 *>(dst) = q;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (p0 + e >= it.lo && p0 + e < it.hi) dst[e] = (uint8_t)(q[e >> 2] >> (8 * (e & 3)));
+    }
   } else {
+    uint16_t *dst = a.v_pool + off;
+    if (whole) {
+      store_u32x4(dst, w);
+    } else {
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (p0 + e >= it.lo && p0 + e < it.hi) dst[e] = sv[s0 + e][d];
+      for (int e = 0; e < 8; ++e)
+        if (p0 + e >= it.lo && p0 + e < it.hi) dst[e] = sv[s0 + e][d];
+    }
   }
 }
 

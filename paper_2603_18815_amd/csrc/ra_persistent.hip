@@ -100,9 +100,15 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m, p
       g = (int)(bg % w.hkv);
       it = pwrite::write_item(w, (int)(item % write_chunks), (int)(bg / w.hkv));
     }
-    if (it.active) pwrite::write_phase1(w, it, g, t, sv[part]);
-    __syncthreads();
-    if (it.active) pwrite::write_phase2(w, it, g, t, sv[part]);
+    if (w.fp8) {
+      if (it.active) pwrite::write_phase1<true>(w, it, g, t, sv[part]);
+      __syncthreads();
+      if (it.active) pwrite::write_phase2<true>(w, it, g, t, sv[part]);
+    } else {
+      if (it.active) pwrite::write_phase1<false>(w, it, g, t, sv[part]);
+      __syncthreads();
+      if (it.active) pwrite::write_phase2<false>(w, it, g, t, sv[part]);
+    }
     return;
   }
   __shared__ int count[kCostBuckets];   // rows per key-block count, then write cursors
@@ -298,10 +304,8 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   m.qblocks = layout.qblocks;
 
   // the fused page write (append rows only): the chunks' tokens at ctx_lens
-  pwrite::WriteArgs w{k_new,         v_new,          cu_q,        ctx_lens,
-                      kv_append.k_pool, kv_append.v_pool, kv_append.block_table,
-                      kv_append.bt_stride, kv_append.num_pages, kv_append.hkv,
-                      total_q,       max_q_len,      max_kv_len_append};
+  const pwrite::WriteArgs w = pwrite::write_args(k_new, v_new, cu_q, ctx_lens, kv_append, total_q,
+                                                 max_q_len, max_kv_len_append);
   const int32_t write_chunks = k_new ? (max_q_len + kPage - 1) / kPage + 1 : 0;
   const int64_t write_blocks =
       ((int64_t)B_append * kv_append.hkv * write_chunks + 3) / (kPlanThreads / pwrite::kItemThreads);

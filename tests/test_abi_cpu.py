@@ -292,8 +292,11 @@ def test_append_write_validation(lib):
     assert call(_kv(), v=None) == _lib.RA_ERR_NULL
     assert call(_kv(), max_kv=100) == _lib.RA_ERR_SHAPE
     assert call(_kv(), Hq=5) == _lib.RA_ERR_SHAPE
-    assert call(_kv(kv_dtype=_lib.RA_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0)) == \
-        _lib.RA_ERR_UNSUPPORTED
+    # fp8 pools are accepted (their scales are validated like everywhere else)
+    fp8 = dict(kv_dtype=_lib.RA_KV_FP8_E4M3, v_scale=1.0)
+    assert call(_kv(k_scale=0.0, **fp8)) == _lib.RA_ERR_SHAPE
+    assert call(_kv(k_scale=1.0, **fp8), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
+    assert call(_kv(k_scale=1.0, **fp8), total_q=0, ws=None) == _lib.RA_OK
     assert call(_kv(), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
     assert call(_kv(), total_q=0, ws=None) == _lib.RA_OK
 
