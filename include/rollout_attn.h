@@ -27,7 +27,9 @@
  *     Concurrent calls on different streams are safe if their outputs and
  *     workspaces do not overlap.
  *   - Every function returns an ra_status. Arguments the host can check are
- *     checked before any HIP call. Nothing aborts.
+ *     checked before any HIP call. Nothing aborts. A softmax or logit `scale`
+ *     must be finite (any sign; 0 weighs every key equally), else
+ *     RA_ERR_SHAPE.
  *   - Zero work (B == 0, total_q == 0, total_new == 0) returns RA_OK without
  *     launching anything.
  *   - Device-resident metadata (lengths, block tables, cu_* offsets) is a
@@ -104,8 +106,9 @@ typedef struct {
   int32_t page_size;          /* must be 16 */
   int32_t head_dim;           /* must be 128 */
   int32_t kv_dtype;           /* ra_kv_dtype of both pools */
-  float k_scale, v_scale;     /* fp8 pools: finite and > 0 (RA_ERR_SHAPE otherwise);
-                                 ignored for bf16 pools */
+  float k_scale, v_scale;     /* fp8 pools: finite, > 0 and with a finite fp32
+                                 reciprocal (RA_ERR_SHAPE otherwise); ignored for
+                                 bf16 pools */
 } ra_paged_kv;
 
 /* ABI version of the loaded library (RA_ABI_VERSION). */

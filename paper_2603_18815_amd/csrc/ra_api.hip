@@ -12,6 +12,8 @@ constexpr int32_t kMaxGridYZ = 65535;
 
 bool valid_status(int s) { return s >= RA_OK && s <= RA_ERR_HIP; }
 
+bool valid_pool_scale(float s) { return std::isfinite(s) && s > 0.f && std::isfinite(1.0f / s); }
+
 // Common checks on the paged cache descriptor.
 int check_kv(const ra_paged_kv *kv) {
   if (!kv) return RA_ERR_NULL;
@@ -19,9 +21,10 @@ int check_kv(const ra_paged_kv *kv) {
   if (kv->num_kv_heads <= 0 || kv->num_pages <= 0 || kv->bt_stride <= 0) return RA_ERR_SHAPE;
   if (kv->num_kv_heads > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
   if (kv->kv_dtype != RA_KV_BF16 && kv->kv_dtype != RA_KV_FP8_E4M3) return RA_ERR_UNSUPPORTED;
-  if (kv->kv_dtype == RA_KV_FP8_E4M3 &&
-      !(std::isfinite(kv->k_scale) && kv->k_scale > 0.f && std::isfinite(kv->v_scale) &&
-        kv->v_scale > 0.f))
+  // fp8 scales: finite, positive, and with a finite fp32 reciprocal (the
+  // page write multiplies by it)
+  if (kv->kv_dtype == RA_KV_FP8_E4M3 && !(valid_pool_scale(kv->k_scale) &&
+                                          valid_pool_scale(kv->v_scale)))
     return RA_ERR_SHAPE;
   if (!kv->k_pool || !kv->v_pool || !kv->block_table) return RA_ERR_NULL;
   return RA_OK;
@@ -70,7 +73,7 @@ size_t rollout_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
 int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_lens, int32_t B,
                         int32_t Hq, int32_t max_kv_len, float scale, float *out, float *lse,
                         void *workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (B < 0 || Hq <= 0 || max_kv_len < 0) return RA_ERR_SHAPE;
+  if (B < 0 || Hq <= 0 || max_kv_len < 0 || !std::isfinite(scale)) return RA_ERR_SHAPE;
   int s = check_kv(kv);
   if (s != RA_OK) return s;
   if (!q || !kv_lens || !out) return RA_ERR_NULL;
@@ -102,7 +105,7 @@ int rollout_attn_decode_shared_prefix(const void *q, const ra_paged_kv *kv,
                                       float *out, float *lse, void *workspace,
                                       size_t workspace_bytes, hipStream_t stream) {
   if (B < 0 || Hq <= 0 || max_kv_len < 0 || num_groups < 0 || max_group_rows < 0 ||
-      max_prefix_len < 0)
+      max_prefix_len < 0 || !std::isfinite(scale))
     return RA_ERR_SHAPE;
   int s = check_kv(kv);
   if (s != RA_OK) return s;
@@ -138,7 +141,8 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                         int32_t max_q_len, int32_t max_kv_len, float scale, float *out,
                         float *lse, void *workspace, size_t workspace_bytes,
                         hipStream_t stream) {
-  if (B < 0 || Hq <= 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0) return RA_ERR_SHAPE;
+  if (B < 0 || Hq <= 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0 || !std::isfinite(scale))
+    return RA_ERR_SHAPE;
   int s = check_kv(kv);
   if (s != RA_OK) return s;
   if (!q || !cu_q || !ctx_lens || !out) return RA_ERR_NULL;
@@ -163,7 +167,8 @@ int rollout_attn_append_write(const void *q, const void *k_new, const void *v_ne
                               int32_t B, int32_t Hq, int32_t total_q, int32_t max_q_len,
                               int32_t max_kv_len, float scale, float *out, float *lse,
                               void *workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (B < 0 || Hq <= 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0) return RA_ERR_SHAPE;
+  if (B < 0 || Hq <= 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0 || !std::isfinite(scale))
+    return RA_ERR_SHAPE;
   int s = check_kv(kv);
   if (s != RA_OK) return s;
   if (!q || !k_new || !v_new || !cu_q || !ctx_lens || !out) return RA_ERR_NULL;
@@ -210,7 +215,7 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
                        int32_t Hq, float scale, void *workspace, size_t workspace_bytes,
                        hipStream_t stream) {
   if (B_decode < 0 || B_append < 0 || Hq <= 0 || max_kv_len_decode < 0 || total_q < 0 ||
-      max_q_len < 0 || max_kv_len_append < 0)
+      max_q_len < 0 || max_kv_len_append < 0 || !std::isfinite(scale))
     return RA_ERR_SHAPE;
   const bool dec = B_decode > 0;
   const bool app = B_append > 0 && total_q > 0 && max_q_len > 0;
@@ -262,7 +267,7 @@ size_t token_logprob_workspace_size(int32_t N, int32_t V) {
 int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t N, int32_t V,
                   int32_t D, float scale, float *logprob, float *lse, void *workspace,
                   size_t workspace_bytes, hipStream_t stream) {
-  if (N < 0 || V <= 0 || D <= 0) return RA_ERR_SHAPE;
+  if (N < 0 || V <= 0 || D <= 0 || !std::isfinite(scale)) return RA_ERR_SHAPE;
   if (!h || !W || !targets || !logprob) return RA_ERR_NULL;
   if (D % 64 != 0) return RA_ERR_UNSUPPORTED;
   if (N == 0) return RA_OK;
@@ -291,7 +296,7 @@ int token_logprob_pack_weight(const void *W, int32_t V, int32_t D, void *W_packe
 int token_logprob_packed(const void *h, const void *W_packed, const int32_t *targets, int32_t N,
                          int32_t V, int32_t D, float scale, float *logprob, float *lse,
                          void *workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (N < 0 || V <= 0 || D <= 0) return RA_ERR_SHAPE;
+  if (N < 0 || V <= 0 || D <= 0 || !std::isfinite(scale)) return RA_ERR_SHAPE;
   if (!h || !W_packed || !targets || !logprob) return RA_ERR_NULL;
   if (D % 64 != 0) return RA_ERR_UNSUPPORTED;
   if (N == 0) return RA_OK;

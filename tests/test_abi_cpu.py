@@ -262,7 +262,7 @@ def test_fp8_pool_validation(lib):
     take fp8 pools are rejected before any launch."""
     fp8 = dict(kv_dtype=_lib.RA_KV_FP8_E4M3, k_scale=0.5, v_scale=2.0)
     assert _decode(lib, _kv(kv_dtype=7)) == _lib.RA_ERR_UNSUPPORTED
-    for bad in (0.0, -1.0, float("inf"), float("nan")):
+    for bad in (0.0, -1.0, float("inf"), float("nan"), 1e-39):   # 1e-39: 1 / scale overflows
         assert _decode(lib, _kv(**dict(fp8, k_scale=bad))) == _lib.RA_ERR_SHAPE
         assert _decode(lib, _kv(**dict(fp8, v_scale=bad))) == _lib.RA_ERR_SHAPE
     assert _decode(lib, _kv(**fp8), ws_bytes=16) == _lib.RA_ERR_WORKSPACE   # fp8 decode passes
@@ -277,6 +277,28 @@ def test_fp8_pool_validation(lib):
     assert _mixed(lib, _kv(**fp8), _kv(**fp8), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
     # the bf16 scales are ignored
     assert _decode(lib, _kv(k_scale=0.0, v_scale=float("nan")), B=0) == _lib.RA_OK
+
+
+def test_nonfinite_scale_rejected(lib):
+    """Every entry point that takes a softmax or logit scale rejects a
+    non-finite one before any launch (finite scales of any sign pass)."""
+    for bad in (float("inf"), float("-inf"), float("nan")):
+        assert _decode(lib, _kv(), scale=bad) == _lib.RA_ERR_SHAPE
+        assert lib.rollout_attn_append(FAKE, FAKE, FAKE, ctypes.byref(_kv()), 2, 4, 10, 5, 64,
+                                       bad, FAKE, None, FAKE, 1 << 30, None) == _lib.RA_ERR_SHAPE
+        assert lib.rollout_attn_append_write(FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.byref(_kv()),
+                                             2, 4, 10, 5, 64, bad, FAKE, None, FAKE, 1 << 30,
+                                             None) == _lib.RA_ERR_SHAPE
+        assert lib.rollout_attn_decode_shared_prefix(
+            FAKE, ctypes.byref(_kv()), FAKE, FAKE, FAKE, 16, 4, 2, 8, 32, 64, bad, FAKE, None,
+            FAKE, 1 << 30, None) == _lib.RA_ERR_SHAPE
+        assert _mixed(lib, _kv(), _kv(), scale=bad) == _lib.RA_ERR_SHAPE
+        assert lib.token_logprob(FAKE, FAKE, FAKE, 8, 100, 128, bad, FAKE, None, FAKE, 1 << 30,
+                                 None) == _lib.RA_ERR_SHAPE
+        assert lib.token_logprob_packed(FAKE, FAKE, FAKE, 8, 100, 128, bad, FAKE, None, FAKE,
+                                        1 << 30, None) == _lib.RA_ERR_SHAPE
+    for ok in (0.0, -0.5):
+        assert _decode(lib, _kv(), scale=ok, B=0) == _lib.RA_OK
 
 
 def test_append_write_validation(lib):
