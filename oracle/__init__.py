@@ -69,6 +69,11 @@ def _load():
     lib.oracle_e4m3_decode.restype = None
     lib.oracle_e4m3_encode.argtypes = [_f64p, c_i64, _u8p]
     lib.oracle_e4m3_encode.restype = None
+    lib.oracle_rope_bf16.argtypes = [_u16p, c_i64, c_int, _i32p,
+                                     np.ctypeslib.ndpointer(dtype=np.float32,
+                                                            flags="C_CONTIGUOUS"),
+                                     c_i64, _u16p]
+    lib.oracle_rope_bf16.restype = c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = c_int
     _lib = lib
@@ -308,3 +313,19 @@ def append_fp8(q, cu_q, ctx_lens, k_pool, v_pool, k_scale, v_scale, block_table,
     if rc != 0:
         raise RuntimeError(f"oracle_append_fp8_f64 failed ({rc})")
     return out, lse
+
+
+def rope(x, positions, cos_sin):
+    """Rows x (bf16 bits [N][H][128]) rotated at positions [N] with the rotary table
+    cos_sin (fp32 [rows][128]: cos | sin), as bf16 bits (see attn_oracle.c)."""
+    lib = _load()
+    x = _u16(x)
+    N, H, D = x.shape
+    assert D == 128
+    pos = _i32(positions).reshape(-1)
+    assert pos.shape[0] == N
+    cs = np.ascontiguousarray(np.asarray(cos_sin, np.float32))
+    out = np.empty_like(x)
+    if lib.oracle_rope_bf16(x, N, H, pos, cs, cs.shape[0], out) != 0:
+        raise ValueError("rope: a position lies outside the table")
+    return out

@@ -396,4 +396,47 @@ int oracle_page_gather_u8(const uint8_t *k_pool, const uint8_t *v_pool,
 }
 
 /* Threads an OpenMP parallel region of the oracle uses (for reporting). */
+/*
+ * Rotary position embedding of token rows (a reading: the paper does not
+ * describe model internals; models of its kind rotate each query and key by
+ * its position). Row x (128 dims) at position p, table row cs = cos_sin[p]
+ * holding c_i = cs[i] and s_i = cs[64 + i] for i < 64:
+ *   y_i = fp32(x_i c_i) - fp32(x_{i+64} s_i),  y_{i+64} = fp32(x_{i+64} c_i) + fp32(x_i s_i),
+ * each product and sum rounded to fp32 (the build disables contraction), the
+ * result rounded to bf16 (nearest even). The rounding to bf16 decides the
+ * stored value, so it is taken in the precision the library states for it.
+ * x, out: bf16 [n_rows][heads][128]; pos: [n_rows]; cos_sin: fp32 [rope_rows][128].
+ * Returns -1 (nothing written) if a position lies outside the table.
+ */
+static uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);   /* quiet NaN */
+  const uint32_t lsb = (u >> 16) & 1u;
+  return (uint16_t)((u + 0x7fffu + lsb) >> 16);
+}
+
+int oracle_rope_bf16(const uint16_t *x, int64_t n_rows, int heads, const int32_t *pos,
+                     const float *cos_sin, int64_t rope_rows, uint16_t *out) {
+  const int D = 128, H = 64;
+  for (int64_t r = 0; r < n_rows; ++r)
+    if (pos[r] < 0 || pos[r] >= rope_rows) return -1;
+  for (int64_t r = 0; r < n_rows; ++r) {
+    const float *cs = cos_sin + (size_t)pos[r] * D;
+    for (int h = 0; h < heads; ++h) {
+      const uint16_t *xr = x + ((size_t)r * heads + h) * D;
+      uint16_t *yr = out + ((size_t)r * heads + h) * D;
+      for (int i = 0; i < H; ++i) {
+        const float lo = (float)bf16_to_f64(xr[i]), hi = (float)bf16_to_f64(xr[i + H]);
+        const float c = cs[i], s = cs[H + i];
+        const float a = lo * c, b = hi * s, a2 = hi * c, b2 = lo * s;
+        const float y_lo = a - b, y_hi = a2 + b2;
+        yr[i] = f32_to_bf16_rne(y_lo);
+        yr[i + H] = f32_to_bf16_rne(y_hi);
+      }
+    }
+  }
+  return 0;
+}
+
 int oracle_num_threads(void) { return omp_get_max_threads(); }

@@ -555,3 +555,76 @@ def test_fp8_scale_laws():
     b, lb = oracle.decode_fp8(q, kp, vp, 1.0, 1.0, bt, lens, 0.003)
     np.testing.assert_allclose(a, 1.7 * b, rtol=1e-12, atol=1e-12)
     np.testing.assert_allclose(la, lb, rtol=1e-12, atol=1e-12)
+
+
+def _rope_table(theta, positions):
+    """cos | sin of the angles p * theta^(-2i/128), i < 64, for the given positions
+    (fp64 math, stored fp32): the table a caller builds for its model."""
+    inv = float(theta) ** (-2.0 * np.arange(64) / 128.0)
+    ang = np.asarray(positions, np.float64)[:, None] * inv[None, :]
+    return np.concatenate([np.cos(ang), np.sin(ang)], axis=1).astype(np.float32)
+
+
+def test_rope_identity_at_angle_zero():
+    """Position 0 (cos 1, sin 0) leaves every row bit for bit."""
+    rng = np.random.default_rng(21)
+    x = randn_bits(rng, (7, 3, 128))
+    table = _rope_table(1e6, np.arange(8))
+    np.testing.assert_array_equal(oracle.rope(x, np.zeros(7, np.int32), table), x)
+
+
+def test_rope_is_the_complex_rotation_of_dim_pairs():
+    """Dims i and i + 64 form the complex number x_i + j x_{i+64}, multiplied by
+    e^{j angle_i}: the rotation computed as a complex product in fp64 agrees with
+    the oracle to within one bf16 step everywhere and exactly almost everywhere
+    (the oracle rounds its products to fp32 first). A swapped pairing
+    (2i, 2i+1) or a flipped sign fails."""
+    rng = np.random.default_rng(22)
+    N, H = 64, 4
+    x = randn_bits(rng, (N, H, 128))
+    table = _rope_table(1e4, np.arange(5000))
+    pos = rng.integers(0, 5000, N).astype(np.int32)
+    y = bits_f64(oracle.rope(x, pos, table))
+    xf = bits_f64(x)
+    c = table[pos, :64].astype(np.float64)[:, None, :]
+    s = table[pos, 64:].astype(np.float64)[:, None, :]
+    z = (xf[..., :64] + 1j * xf[..., 64:]) * (c + 1j * s)
+    ref = np.concatenate([z.real, z.imag], axis=-1)
+    ulp = np.abs(bits_f64(bf16_bits(ref))) * 2.0 ** -7 + 1e-30
+    err = np.abs(y - ref)
+    assert np.all(err <= ulp + 1e-12)
+    assert np.mean(y == bits_f64(bf16_bits(ref))) > 0.99
+
+
+def test_rope_scores_depend_on_relative_position_only():
+    """<rot(q, p1), rot(k, p2)> is a function of p1 - p2: shifting both
+    positions by d changes it only by bf16 rounding."""
+    rng = np.random.default_rng(23)
+    q = randn_bits(rng, (1, 1, 128))
+    k = randn_bits(rng, (1, 1, 128))
+    table = _rope_table(1e6, np.arange(40000))
+    for p1, p2, d in [(5, 3, 1000), (30000, 17, 7777), (100, 9000, 20000)]:
+        a = np.sum(bits_f64(oracle.rope(q, [p1], table)) * bits_f64(oracle.rope(k, [p2], table)))
+        b = np.sum(bits_f64(oracle.rope(q, [p1 + d], table)) *
+                   bits_f64(oracle.rope(k, [p2 + d], table)))
+        assert abs(a - b) < 0.1, (p1, p2, d, a, b)
+    # and it does change with the relative position
+    a = np.sum(bits_f64(oracle.rope(q, [5], table)) * bits_f64(oracle.rope(k, [3], table)))
+    b = np.sum(bits_f64(oracle.rope(q, [5], table)) * bits_f64(oracle.rope(k, [30003], table)))
+    assert abs(a - b) > 0.5
+
+
+def test_rope_inverse_rotation_and_pair_norms():
+    """Rotating by an angle and then by its negative returns the row (to bf16
+    rounding), and each pair's norm is kept."""
+    rng = np.random.default_rng(24)
+    x = randn_bits(rng, (16, 2, 128))
+    p = 12345.0
+    table = _rope_table(1e4, [0.0, p, -p])
+    y = oracle.rope(x, np.ones(16, np.int32), table)
+    back = oracle.rope(y, np.full(16, 2, np.int32), table)
+    np.testing.assert_allclose(bits_f64(back), bits_f64(x), rtol=2 ** -6, atol=2 ** -7)
+    xf, yf = bits_f64(x), bits_f64(y)
+    n0 = xf[..., :64] ** 2 + xf[..., 64:] ** 2
+    n1 = yf[..., :64] ** 2 + yf[..., 64:] ** 2
+    np.testing.assert_allclose(n1, n0, rtol=2 ** -6, atol=1e-3)
