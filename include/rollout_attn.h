@@ -42,7 +42,7 @@
  *   - Results are deterministic: the same inputs give bitwise the same
  *     outputs, independent of which physical pages the block table names.
  *
- * Paged KV layout (ABI versions 2 and 3). Page size P = 16 tokens, head dim D = 128.
+ * Paged KV layout (ABI versions 2 to 4). Page size P = 16 tokens, head dim D = 128.
  * Logical token j of row b lives in physical page bt[b * bt_stride + j / P]
  * at slot j % P. Within a page each KV head owns one contiguous block:
  *   K pool  [num_pages][Hkv][P][D]   element (page, g, slot, d) at
@@ -78,7 +78,7 @@
 extern "C" {
 #endif
 
-#define RA_ABI_VERSION 3
+#define RA_ABI_VERSION 4
 #define RA_PAGE_SIZE 16
 #define RA_HEAD_DIM 128
 
@@ -249,6 +249,45 @@ int rollout_attn_append_write(const void *q, const void *k_new, const void *v_ne
                               int32_t B, int32_t Hq, int32_t total_q, int32_t max_q_len,
                               int32_t max_kv_len, float scale, float *out, float *lse,
                               void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Rotary position embedding on write. Models of the paper's kind (e.g. Qwen3)
+ * rotate each query and key by its position before attention; the paper does
+ * not describe model internals, so the rotation is an option of the write
+ * path: the key is rotated as it is written into its page, and in the fused
+ * call the chunk's queries are rotated as they are loaded.
+ *
+ * Rotation of a 128-dim head row x at position p with the table cos_sin
+ * (fp32 [rope_rows][128]; row p holds c_i = cos(p w_i) in columns 0..63 and
+ * s_i = sin(p w_i) in columns 64..127, computed by the caller for its model's
+ * frequencies w_i), for i in [0, 64):
+ *   y_i      = fp32(x_i c_i) - fp32(x_{i+64} s_i)
+ *   y_{i+64} = fp32(x_{i+64} c_i) + fp32(x_i s_i)
+ * each product and each sum rounded to fp32 (no fused multiply-add), then y
+ * rounded to bf16 (nearest even). The rotated bf16 row is what is written
+ * (bit copy, or E4M3 quantization for fp8 pools, exactly as kv_page_write
+ * writes a bf16 row) and what the attention uses.
+ *
+ * kv_page_write_rope: kv_page_write with the keys rotated at their positions
+ *   start_pos[b] + t (values unrotated). Needs max_pos <= rope_rows.
+ * rollout_attn_append_write_rope: rollout_attn_append_write with the chunk's
+ *   keys rotated at ctx_lens[b] + i as they are written and its queries
+ *   rotated at the same positions; equal, bitwise, to kv_page_write_rope
+ *   followed by rollout_attn_append on the rotated queries. Needs
+ *   max_kv_len <= rope_rows.
+ * Errors: as the unrotated calls; RA_ERR_NULL (cos_sin NULL); RA_ERR_SHAPE
+ * (rope_rows <= 0 or too few rows).
+ */
+int kv_page_write_rope(const void *k_new, const void *v_new, const int32_t *cu_new,
+                       const int32_t *start_pos, const ra_paged_kv *kv, int32_t B,
+                       int32_t total_new, int32_t max_new, int32_t max_pos, const float *cos_sin,
+                       int32_t rope_rows, hipStream_t stream);
+int rollout_attn_append_write_rope(const void *q, const void *k_new, const void *v_new,
+                                   const int32_t *cu_q, const int32_t *ctx_lens,
+                                   const ra_paged_kv *kv, int32_t B, int32_t Hq, int32_t total_q,
+                                   int32_t max_q_len, int32_t max_kv_len, float scale,
+                                   const float *cos_sin, int32_t rope_rows, float *out, float *lse,
+                                   void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Mixed step: the attention of one rollout step in which some trajectories

@@ -262,10 +262,13 @@ def append_write(q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, cu_q
                  ctx_lens: torch.Tensor, kv: PagedKV, max_q_len: Optional[int] = None,
                  max_kv_len: Optional[int] = None, scale: Optional[float] = None,
                  out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-                 want_lse: bool = False, workspace: Optional[torch.Tensor] = None, stream=None
+                 want_lse: bool = False, workspace: Optional[torch.Tensor] = None, stream=None,
+                 cos_sin: Optional[torch.Tensor] = None
                  ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
     """Write the chunks' K/V (bf16 [total_q][Hkv][128], packed like q) at positions
-    ctx_lens[b] + i and run the append attention, in one launch."""
+    ctx_lens[b] + i and run the append attention, in one launch. With a rotary table
+    cos_sin (fp32 [rows][128]) the chunk's keys and queries are rotated at their
+    positions."""
     lib = _lib.load()
     dev = kv.device
     for t, n in ((q, "q"), (k_new, "k_new"), (v_new, "v_new")):
@@ -301,10 +304,19 @@ def append_write(q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, cu_q
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     _need(workspace, "workspace", torch.uint8, dev)
     s = kv.struct()
-    _lib.check("rollout_attn_append_write", lib.rollout_attn_append_write(
-        q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), cu_q.data_ptr(), ctx_lens.data_ptr(),
-        ctypes.byref(s), B, Hq, total_q, max_q_len, max_kv_len, float(scale), out.data_ptr(),
-        _ptr(lse), workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
+    if cos_sin is None:
+        _lib.check("rollout_attn_append_write", lib.rollout_attn_append_write(
+            q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), cu_q.data_ptr(),
+            ctx_lens.data_ptr(), ctypes.byref(s), B, Hq, total_q, max_q_len, max_kv_len,
+            float(scale), out.data_ptr(), _ptr(lse), workspace.data_ptr(), workspace.numel(),
+            _stream(dev, stream)))
+    else:
+        rows = _rope_table(cos_sin, dev)
+        _lib.check("rollout_attn_append_write_rope", lib.rollout_attn_append_write_rope(
+            q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), cu_q.data_ptr(),
+            ctx_lens.data_ptr(), ctypes.byref(s), B, Hq, total_q, max_q_len, max_kv_len,
+            float(scale), cos_sin.data_ptr(), rows, out.data_ptr(), _ptr(lse),
+            workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
     return out, lse
 
 
@@ -387,11 +399,22 @@ def mixed(q_decode: torch.Tensor, kv_decode: PagedKV, kv_lens: torch.Tensor,
     return out_decode, out_append, lse_d, lse_a
 
 
+def _rope_table(cos_sin: torch.Tensor, dev) -> int:
+    """Checks a rotary table (fp32 [rows][128]: cos | sin) and returns its rows."""
+    _need(cos_sin, "cos_sin", torch.float32, dev)
+    if cos_sin.dim() != 2 or cos_sin.shape[1] != HEAD_DIM:
+        raise ValueError(f"cos_sin must have shape [rows][{HEAD_DIM}], got {tuple(cos_sin.shape)}")
+    return int(cos_sin.shape[0])
+
+
 def kv_page_write(k_new: torch.Tensor, v_new: torch.Tensor, cu_new: torch.Tensor,
                   start_pos: torch.Tensor, kv: PagedKV, max_new: Optional[int] = None,
-                  max_pos: Optional[int] = None, stream=None) -> None:
+                  max_pos: Optional[int] = None, stream=None,
+                  cos_sin: Optional[torch.Tensor] = None) -> None:
     """Scatter packed new tokens (bf16 [N][Hkv][128]) into the pages (a bit copy into
-    bf16 pools, quantized to E4M3 codes in fp8 pools)."""
+    bf16 pools, quantized to E4M3 codes in fp8 pools). With a rotary table cos_sin
+    (fp32 [rows][128], cos | sin per position) the keys are rotated at their
+    positions as they are written."""
     lib = _lib.load()
     dev = kv.device
     _need(k_new, "k_new", torch.bfloat16, dev)
@@ -410,9 +433,16 @@ def kv_page_write(k_new: torch.Tensor, v_new: torch.Tensor, cu_new: torch.Tensor
         if max_pos is None:
             max_pos = int((n + start_pos).max().item()) if B else 0
     s = kv.struct()
-    _lib.check("kv_page_write", lib.kv_page_write(
-        k_new.data_ptr(), v_new.data_ptr(), cu_new.data_ptr(), start_pos.data_ptr(),
-        ctypes.byref(s), B, k_new.shape[0], max_new, max_pos, _stream(dev, stream)))
+    if cos_sin is None:
+        _lib.check("kv_page_write", lib.kv_page_write(
+            k_new.data_ptr(), v_new.data_ptr(), cu_new.data_ptr(), start_pos.data_ptr(),
+            ctypes.byref(s), B, k_new.shape[0], max_new, max_pos, _stream(dev, stream)))
+    else:
+        rows = _rope_table(cos_sin, dev)
+        _lib.check("kv_page_write_rope", lib.kv_page_write_rope(
+            k_new.data_ptr(), v_new.data_ptr(), cu_new.data_ptr(), start_pos.data_ptr(),
+            ctypes.byref(s), B, k_new.shape[0], max_new, max_pos, cos_sin.data_ptr(), rows,
+            _stream(dev, stream)))
 
 
 def kv_page_gather(kv: PagedKV, lens: torch.Tensor, cu_out: torch.Tensor,

@@ -25,9 +25,11 @@ EXPORTS = (
     "rollout_attn_append_workspace_size",
     "rollout_attn_append",
     "rollout_attn_append_write",
+    "rollout_attn_append_write_rope",
     "rollout_attn_mixed_workspace_size",
     "rollout_attn_mixed",
     "kv_page_write",
+    "kv_page_write_rope",
     "kv_page_gather",
     "token_logprob_workspace_size",
     "token_logprob",
@@ -95,6 +97,9 @@ def load() -> ctypes.CDLL:
     lib.rollout_attn_append_write.argtypes = [vp, vp, vp, vp, vp, kvp, i32, i32, i32, i32, i32,
                                               f32, vp, vp, vp, sz, vp]
     lib.rollout_attn_append_write.restype = ctypes.c_int
+    lib.rollout_attn_append_write_rope.argtypes = [vp, vp, vp, vp, vp, kvp, i32, i32, i32, i32,
+                                                   i32, f32, vp, i32, vp, vp, vp, sz, vp]
+    lib.rollout_attn_append_write_rope.restype = ctypes.c_int
     lib.rollout_attn_mixed_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
     lib.rollout_attn_mixed_workspace_size.restype = sz
     lib.rollout_attn_mixed.argtypes = [vp, kvp, vp, i32, i32, vp, vp,
@@ -113,6 +118,8 @@ def load() -> ctypes.CDLL:
     lib.token_logprob_packed.restype = ctypes.c_int
     lib.kv_page_write.argtypes = [vp, vp, vp, vp, kvp, i32, i32, i32, i32, vp]
     lib.kv_page_write.restype = ctypes.c_int
+    lib.kv_page_write_rope.argtypes = [vp, vp, vp, vp, kvp, i32, i32, i32, i32, vp, i32, vp]
+    lib.kv_page_write_rope.restype = ctypes.c_int
     lib.kv_page_gather.argtypes = [kvp, vp, vp, i32, i32, i32, vp, vp, vp]
     lib.kv_page_gather.restype = ctypes.c_int
     _lib = lib

@@ -162,11 +162,17 @@ int rollout_attn_append(const void *q, const int32_t *cu_q, const int32_t *ctx_l
                                      workspace, layout, stream));
 }
 
-int rollout_attn_append_write(const void *q, const void *k_new, const void *v_new,
-                              const int32_t *cu_q, const int32_t *ctx_lens, const ra_paged_kv *kv,
-                              int32_t B, int32_t Hq, int32_t total_q, int32_t max_q_len,
-                              int32_t max_kv_len, float scale, float *out, float *lse,
-                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// rollout_attn_append_write, with an optional rotary table (cos_sin null: none;
+// otherwise checked by the caller).
+int append_write_impl(const void *q, const void *k_new, const void *v_new, const int32_t *cu_q,
+                      const int32_t *ctx_lens, const ra_paged_kv *kv, int32_t B, int32_t Hq,
+                      int32_t total_q, int32_t max_q_len, int32_t max_kv_len, float scale,
+                      const float *cos_sin, int32_t rope_rows, float *out, float *lse,
+                      void *workspace, size_t workspace_bytes, hipStream_t stream) {
   if (B < 0 || Hq <= 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0 || !std::isfinite(scale))
     return RA_ERR_SHAPE;
   int s = check_kv(kv);
@@ -188,7 +194,60 @@ int rollout_attn_append_write(const void *q, const void *k_new, const void *v_ne
   return hip_status(ra::launch_mixed(
       nullptr, k, nullptr, 0, 0, nullptr, nullptr, static_cast<const uint16_t *>(q), cu_q,
       ctx_lens, k, B, total_q, max_q_len, max_kv_len, out, lse, Hq, scale, workspace, layout,
-      stream, static_cast<const uint16_t *>(k_new), static_cast<const uint16_t *>(v_new)));
+      stream, static_cast<const uint16_t *>(k_new), static_cast<const uint16_t *>(v_new), cos_sin,
+      rope_rows));
+}
+
+// kv_page_write, with an optional rotary table for K.
+int page_write_impl(const void *k_new, const void *v_new, const int32_t *cu_new,
+                    const int32_t *start_pos, const ra_paged_kv *kv, int32_t B, int32_t total_new,
+                    int32_t max_new, int32_t max_pos, const float *cos_sin, int32_t rope_rows,
+                    hipStream_t stream) {
+  if (B < 0 || total_new < 0 || max_new < 0 || max_pos < 0) return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!k_new || !v_new || !cu_new || !start_pos) return RA_ERR_NULL;
+  if (B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_pos) || max_new > max_pos) return RA_ERR_SHAPE;
+  if (B == 0 || total_new == 0 || max_new == 0) return RA_OK;
+  return hip_status(ra::launch_page_write(static_cast<const uint16_t *>(k_new),
+                                          static_cast<const uint16_t *>(v_new), cu_new, start_pos,
+                                          to_internal(kv), B, total_new, max_new, max_pos, stream,
+                                          cos_sin, rope_rows));
+}
+
+// A rotary table must cover every position the call uses: [0, max_pos).
+int check_rope(const float *cos_sin, int32_t rope_rows, int32_t max_pos) {
+  if (rope_rows <= 0 || max_pos > rope_rows) return RA_ERR_SHAPE;
+  if (!cos_sin) return RA_ERR_NULL;
+  return RA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rollout_attn_append_write(const void *q, const void *k_new, const void *v_new,
+                              const int32_t *cu_q, const int32_t *ctx_lens, const ra_paged_kv *kv,
+                              int32_t B, int32_t Hq, int32_t total_q, int32_t max_q_len,
+                              int32_t max_kv_len, float scale, float *out, float *lse,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  return append_write_impl(q, k_new, v_new, cu_q, ctx_lens, kv, B, Hq, total_q, max_q_len,
+                           max_kv_len, scale, nullptr, 0, out, lse, workspace, workspace_bytes,
+                           stream);
+}
+
+int rollout_attn_append_write_rope(const void *q, const void *k_new, const void *v_new,
+                                   const int32_t *cu_q, const int32_t *ctx_lens,
+                                   const ra_paged_kv *kv, int32_t B, int32_t Hq, int32_t total_q,
+                                   int32_t max_q_len, int32_t max_kv_len, float scale,
+                                   const float *cos_sin, int32_t rope_rows, float *out, float *lse,
+                                   void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  const int r = check_rope(cos_sin, rope_rows, max_kv_len);
+  if (r != RA_OK) return r;
+  return append_write_impl(q, k_new, v_new, cu_q, ctx_lens, kv, B, Hq, total_q, max_q_len,
+                           max_kv_len, scale, cos_sin, rope_rows, out, lse, workspace,
+                           workspace_bytes, stream);
 }
 
 size_t rollout_attn_mixed_workspace_size(int32_t B_decode, int32_t B_append, int32_t Hq,
@@ -310,17 +369,18 @@ int token_logprob_packed(const void *h, const void *W_packed, const int32_t *tar
 int kv_page_write(const void *k_new, const void *v_new, const int32_t *cu_new,
                   const int32_t *start_pos, const ra_paged_kv *kv, int32_t B, int32_t total_new,
                   int32_t max_new, int32_t max_pos, hipStream_t stream) {
-  if (B < 0 || total_new < 0 || max_new < 0 || max_pos < 0) return RA_ERR_SHAPE;
-  int s = check_kv(kv);
-  if (s != RA_OK) return s;
-  if (!k_new || !v_new || !cu_new || !start_pos) return RA_ERR_NULL;
-  if (B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
-  if (!positions_fit(kv, max_pos) || max_new > max_pos) return RA_ERR_SHAPE;
-  if (B == 0 || total_new == 0 || max_new == 0) return RA_OK;
-  return hip_status(ra::launch_page_write(static_cast<const uint16_t *>(k_new),
-                                          static_cast<const uint16_t *>(v_new), cu_new, start_pos,
-                                          to_internal(kv), B, total_new, max_new, max_pos,
-                                          stream));
+  return page_write_impl(k_new, v_new, cu_new, start_pos, kv, B, total_new, max_new, max_pos,
+                         nullptr, 0, stream);
+}
+
+int kv_page_write_rope(const void *k_new, const void *v_new, const int32_t *cu_new,
+                       const int32_t *start_pos, const ra_paged_kv *kv, int32_t B,
+                       int32_t total_new, int32_t max_new, int32_t max_pos, const float *cos_sin,
+                       int32_t rope_rows, hipStream_t stream) {
+  const int r = check_rope(cos_sin, rope_rows, max_pos);
+  if (r != RA_OK) return r;
+  return page_write_impl(k_new, v_new, cu_new, start_pos, kv, B, total_new, max_new, max_pos,
+                         cos_sin, rope_rows, stream);
 }
 
 int kv_page_gather(const ra_paged_kv *kv, const int32_t *lens, const int32_t *cu_out, int32_t B,

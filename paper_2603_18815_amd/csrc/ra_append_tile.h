@@ -57,6 +57,8 @@ struct AppendArgs {
   int32_t hq, hkv, group, bt_stride, num_pages, total_q, max_q_len, max_kv_len, q_per_block;
   float scale_log2;   // softmax scale * log2(e) (* k_scale for fp8 pools)
   float v_scale;      // multiplies the output (fp8 pools; 1 for bf16)
+  const float *cos_sin;   // rotary table [rope_rows][128] for q (kernels built for it)
+  int32_t rope_rows;
 };
 
 // D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16). Lane l supplies A row
@@ -123,7 +125,8 @@ __device__ __forceinline__ int append_tile_blocks(const AppendArgs &a, const App
 // threads. Every thread of the workgroup calls it with the same arguments.
 // kFp8: the pools hold E4M3 codes; the staging converts them exactly to bf16
 // on their way into LDS, so everything after the staging is the bf16 tile.
-template <bool kPosScale, bool kFp8 = false>
+// kRope: q is rotated at its position (table a.cos_sin) after it is loaded.
+template <bool kPosScale, bool kFp8 = false, bool kRope = false>
 __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g, int b,
                                             AppendLds &lds) {
   const int tid = threadIdx.x;
@@ -160,6 +163,20 @@ __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g
   } else {
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) qop[kk] = bf16x8{};
+  }
+  if constexpr (kRope) {
+    // q rotated at its position: the lane's dims 16 kk + 8 grp + 0..7 (kk < 4)
+    // pair with dims 64 + the same, held in qop[kk + 4]
+    const float *cs =
+        a.cos_sin + (size_t)min(max(qpos, 0), a.rope_rows - 1) * kHeadDim + 8 * grp;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const f32x8 c = *reinterpret_cast<const f32x8 *>(cs + 16 * kk);
+      const f32x8 sn = *reinterpret_cast<const f32x8 *>(cs + kHeadDim / 2 + 16 * kk);
+      const bf16x8 lo = qop[kk], hi = qop[kk + 4];
+      qop[kk] = rope8(lo, hi, c, sn, false);
+      qop[kk + 4] = rope8(hi, lo, c, sn, true);
+    }
   }
   // First query position of this wave (its rows are query-major).
   const int wave_q0 = ctx + i0 + (wave * kRowsPerWave) / G;
@@ -405,6 +422,8 @@ inline AppendArgs make_append_args(const uint16_t *q, const int32_t *cu_q,
   a.q_per_block = kRowsPerGroup / a.group;
   a.scale_log2 = scale * kLog2e * kv.k_scale;
   a.v_scale = kv.v_scale;
+  a.cos_sin = nullptr;
+  a.rope_rows = 0;
   return a;
 }
 

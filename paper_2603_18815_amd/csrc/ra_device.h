@@ -47,6 +47,19 @@ __device__ __forceinline__ f32x8 to_f32x8(bf16x8 v) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Rotary position embedding of eight dims of a 128-dim head row, pairing dim
+// i with dim i + 64: for the lower dims (upper = false) x c - y s, for the
+// upper ones x c + y s, where x are the eight dims, y their partners and
+// c, s the cosines and sines of the pairs' angles. Each product and the sum
+// are rounded to fp32 separately (no fused multiply-add), the result to bf16
+// (round to nearest even).
+__device__ __forceinline__ bf16x8 rope8(bf16x8 x, bf16x8 y, f32x8 c, f32x8 s, bool upper) {
+#pragma clang fp contract(off)
+  const f32x8 xf = to_f32x8(x), yf = to_f32x8(y);
+  const f32x8 a = xf * c, b = yf * s;
+  return to_bf16x8(upper ? a + b : a - b);
+}
+
 // Max / sum over the four lanes that share a matrix column (lanes l, l^16,
 // l^32, l^48).
 __device__ __forceinline__ float col_max4(float x) {

@@ -76,7 +76,8 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
                         int32_t max_kv_len_append, float *out_append, float *lse_append,
                         int32_t hq, float scale, void *workspace, const MixedLayout &layout,
                         hipStream_t stream, const uint16_t *k_new = nullptr,
-                        const uint16_t *v_new = nullptr);
+                        const uint16_t *v_new = nullptr, const float *cos_sin = nullptr,
+                        int32_t rope_rows = 0);
 
 // ---- per-token log-probabilities under an LM head ----
 int32_t logprob_chunks(int32_t V);
@@ -93,7 +94,8 @@ hipError_t launch_logprob_pack(const uint16_t *W, int32_t V, int32_t D, uint16_t
 hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
                              const int32_t *start_pos, const PagedKV &kv, int32_t B,
                              int32_t total_new, int32_t max_new, int32_t max_pos,
-                             hipStream_t stream);
+                             hipStream_t stream, const float *cos_sin = nullptr,
+                             int32_t rope_rows = 0);
 
 hipError_t launch_page_gather(const PagedKV &kv, const int32_t *lens, const int32_t *cu_out,
                               int32_t B, int32_t total, int32_t max_len, uint16_t *k_out,

@@ -17,12 +17,12 @@ constexpr int kThreads = 256;
 constexpr int kVPitch = kHeadDim + 8;  // LDS row pitch (elements) of the staged V slots
 
 // One (row, page, KV head) block per workgroup.
-template <bool kFp8>
+template <bool kFp8, bool kRope>
 __global__ __launch_bounds__(pwrite::kItemThreads) void page_write_kernel(pwrite::WriteArgs a) {
   const pwrite::WriteItem it = pwrite::write_item(a, blockIdx.x, blockIdx.z);
   if (!it.active) return;
   __shared__ uint16_t sv[kPage][pwrite::kVPitch];
-  pwrite::write_phase1<kFp8>(a, it, blockIdx.y, threadIdx.x, sv);
+  pwrite::write_phase1<kFp8, kRope>(a, it, blockIdx.y, threadIdx.x, sv);
   __syncthreads();
   pwrite::write_phase2<kFp8>(a, it, blockIdx.y, threadIdx.x, sv);
 }
@@ -96,15 +96,20 @@ __global__ __launch_bounds__(kThreads) void page_gather_fp8_kernel(
 hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
                              const int32_t *start_pos, const PagedKV &kv, int32_t B,
                              int32_t total_new, int32_t max_new, int32_t max_pos,
-                             hipStream_t stream) {
+                             hipStream_t stream, const float *cos_sin, int32_t rope_rows) {
   // A run of n tokens touches at most (n - 1) / 16 + 2 pages.
   const dim3 grid((max_new + kPage - 1) / kPage + 1, kv.hkv, B);
   const pwrite::WriteArgs a = pwrite::write_args(k_new, v_new, cu_new, start_pos, kv, total_new,
-                                                 max_new, max_pos);
-  if (kv.fp8)
-    hipLaunchKernelGGL(page_write_kernel<true>, grid, dim3(pwrite::kItemThreads), 0, stream, a);
+                                                 max_new, max_pos, cos_sin, rope_rows);
+  const dim3 block(pwrite::kItemThreads);
+  if (kv.fp8 && cos_sin)
+    hipLaunchKernelGGL((page_write_kernel<true, true>), grid, block, 0, stream, a);
+  else if (kv.fp8)
+    hipLaunchKernelGGL((page_write_kernel<true, false>), grid, block, 0, stream, a);
+  else if (cos_sin)
+    hipLaunchKernelGGL((page_write_kernel<false, true>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(page_write_kernel<false>, grid, dim3(pwrite::kItemThreads), 0, stream, a);
+    hipLaunchKernelGGL((page_write_kernel<false, false>), grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

@@ -6,6 +6,9 @@
 // stores on the touched slots only).
 // bf16 pools: bit copies. fp8 pools (kFp8): each bf16 element is stored as
 // its E4M3 code of x * fp32(1 / scale) (round to nearest even, saturated).
+// With a rotary table (kRope), each K row is first rotated at its position
+// (rope8: dims i and i + 64 paired, fp32 products and sum, bf16 result) and
+// the rotated row is written as above; V is written as it comes.
 #pragma once
 
 #include "ra_device.h"
@@ -25,13 +28,16 @@ struct WriteArgs {
   int32_t bt_stride, num_pages, hkv, total_new, max_new, max_pos;
   bool fp8;                            // the pools hold E4M3 codes
   float k_inv, v_inv;                  // fp8 pools: fp32(1 / k_scale), fp32(1 / v_scale)
+  const float *cos_sin;                // rotary table [rope_rows][128] (cos | sin), or null
+  int32_t rope_rows;
 };
 
 // Write arguments for pool kv (the reciprocal scales are taken in fp32, as
 // the quantization rule states).
 inline WriteArgs write_args(const uint16_t *k_new, const uint16_t *v_new, const int32_t *cu_new,
                             const int32_t *start_pos, const PagedKV &kv, int32_t total_new,
-                            int32_t max_new, int32_t max_pos) {
+                            int32_t max_new, int32_t max_pos, const float *cos_sin = nullptr,
+                            int32_t rope_rows = 0) {
   WriteArgs a;
   a.k_new = k_new;
   a.v_new = v_new;
@@ -49,6 +55,8 @@ inline WriteArgs write_args(const uint16_t *k_new, const uint16_t *v_new, const 
   a.fp8 = kv.fp8;
   a.k_inv = kv.fp8 ? 1.0f / kv.k_scale : 1.f;
   a.v_inv = kv.fp8 ? 1.0f / kv.v_scale : 1.f;
+  a.cos_sin = cos_sin;
+  a.rope_rows = rope_rows;
   return a;
 }
 
@@ -78,19 +86,31 @@ __device__ __forceinline__ WriteItem write_item(const WriteArgs &a, int chunk, i
 }
 
 // Phase 1 (thread t of 256): K rows to the page, V tokens into LDS.
-template <bool kFp8>
+template <bool kFp8, bool kRope = false>
 __device__ __forceinline__ void write_phase1(const WriteArgs &a, const WriteItem &it, int g,
                                              int t, uint16_t (*sv)[kVPitch]) {
   const int slot = t >> 4, ch = t & 15;            // token slot, 8-element chunk
   const int pos = it.pg * kPage + slot;
   if (pos >= it.lo && pos < it.hi) {
-    const size_t src = ((size_t)(it.cu0 + pos - it.s) * a.hkv + g) * kHeadDim + ch * 8;
+    const size_t row = ((size_t)(it.cu0 + pos - it.s) * a.hkv + g) * kHeadDim;
+    const size_t src = row + ch * 8;
     const size_t dst = (((size_t)it.id * a.hkv + g) * kPage + slot) * kHeadDim + ch * 8;
+    u32x4 k = load_u32x4(a.k_new + src);
+    if constexpr (kRope) {
+      // this chunk's dims 8 ch + 0..7 pair with chunk ch ^ 8; frequency index
+      // 8 (ch % 8) + 0..7
+      const u32x4 partner = load_u32x4(a.k_new + row + (ch ^ 8) * 8);
+      const float *cs = a.cos_sin + (size_t)min(pos, a.rope_rows - 1) * kHeadDim + (ch & 7) * 8;
+      const f32x8 c = *reinterpret_cast<const f32x8 *>(cs);
+      const f32x8 sn = *reinterpret_cast<const f32x8 *>(cs + kHeadDim / 2);
+      k = __builtin_bit_cast(u32x4, rope8(__builtin_bit_cast(bf16x8, k),
+                                          __builtin_bit_cast(bf16x8, partner), c, sn, ch >= 8));
+    }
     if constexpr (kFp8)
       *reinterpret_cast<u32x2 *>(reinterpret_cast<uint8_t *>(a.k_pool) + dst) =
-          quantize8(load_u32x4(a.k_new + src), a.k_inv);
+          quantize8(k, a.k_inv);
     else
-      store_u32x4(a.k_pool + dst, load_u32x4(a.k_new + src));
+      store_u32x4(a.k_pool + dst, k);
     *reinterpret_cast<u32x4 *>(&sv[slot][ch * 8]) = load_u32x4(a.v_new + src);
   }
 }

@@ -100,14 +100,22 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m, p
       g = (int)(bg % w.hkv);
       it = pwrite::write_item(w, (int)(item % write_chunks), (int)(bg / w.hkv));
     }
-    if (w.fp8) {
-      if (it.active) pwrite::write_phase1<true>(w, it, g, t, sv[part]);
-      __syncthreads();
-      if (it.active) pwrite::write_phase2<true>(w, it, g, t, sv[part]);
-    } else {
-      if (it.active) pwrite::write_phase1<false>(w, it, g, t, sv[part]);
-      __syncthreads();
-      if (it.active) pwrite::write_phase2<false>(w, it, g, t, sv[part]);
+    if (it.active) {
+      if (w.fp8 && w.cos_sin)
+        pwrite::write_phase1<true, true>(w, it, g, t, sv[part]);
+      else if (w.fp8)
+        pwrite::write_phase1<true, false>(w, it, g, t, sv[part]);
+      else if (w.cos_sin)
+        pwrite::write_phase1<false, true>(w, it, g, t, sv[part]);
+      else
+        pwrite::write_phase1<false, false>(w, it, g, t, sv[part]);
+    }
+    __syncthreads();
+    if (it.active) {
+      if (w.fp8)
+        pwrite::write_phase2<true>(w, it, g, t, sv[part]);
+      else
+        pwrite::write_phase2<false>(w, it, g, t, sv[part]);
     }
     return;
   }
@@ -221,8 +229,9 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m, p
 }
 
 // kDecode: the call has decode rows (otherwise every entry is an append tile).
-// kFp8: the pools hold E4M3 codes.
-template <bool kPosScale, bool kDecode, bool kFp8>
+// kFp8: the pools hold E4M3 codes. kRope: the append rows' q is rotated at its
+// position (append-only calls).
+template <bool kPosScale, bool kDecode, bool kFp8, bool kRope = false>
 __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
   __shared__ union {
     atile::AppendLds ap;
@@ -251,7 +260,7 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
                                                         e.y >> kHeadBits, e.x, lds.de);
       } else {
         const int2 e = tiles[j - dj];
-        atile::append_tile<kPosScale, kFp8>(m.ap, e.y >> kHeadBits,
+        atile::append_tile<kPosScale, kFp8, kRope>(m.ap, e.y >> kHeadBits,
                                             e.y & ((1 << kHeadBits) - 1), e.x, lds.ap);
       }
     }
@@ -288,11 +297,14 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
                         int32_t B_append, int32_t total_q, int32_t max_q_len,
                         int32_t max_kv_len_append, float *out_append, float *lse_append,
                         int32_t hq, float scale, void *workspace, const MixedLayout &layout,
-                        hipStream_t stream, const uint16_t *k_new, const uint16_t *v_new) {
+                        hipStream_t stream, const uint16_t *k_new, const uint16_t *v_new,
+                        const float *cos_sin, int32_t rope_rows) {
   char *ws = static_cast<char *>(workspace);
   MixedArgs m;
   m.ap = atile::make_append_args(q_append, cu_q, ctx_lens, kv_append, hq, total_q, max_q_len,
                                  max_kv_len_append, scale, out_append, lse_append);
+  m.ap.cos_sin = cos_sin;   // q of the append rows rotated at their positions (or not)
+  m.ap.rope_rows = rope_rows;
   m.de = dsplit::make_decode_args(q_decode, kv_decode, kv_lens, B_decode, hq,
                                   max_kv_len_decode, scale, ws + layout.partials_offset,
                                   layout.plan.max_splits, layout.plan);
@@ -305,7 +317,7 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
 
   // the fused page write (append rows only): the chunks' tokens at ctx_lens
   const pwrite::WriteArgs w = pwrite::write_args(k_new, v_new, cu_q, ctx_lens, kv_append, total_q,
-                                                 max_q_len, max_kv_len_append);
+                                                 max_q_len, max_kv_len_append, cos_sin, rope_rows);
   const int32_t write_chunks = k_new ? (max_q_len + kPage - 1) / kPage + 1 : 0;
   const int64_t write_blocks =
       ((int64_t)B_append * kv_append.hkv * write_chunks + 3) / (kPlanThreads / pwrite::kItemThreads);
@@ -325,20 +337,26 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   const dim3 g(grid), b(kMixThreads);
   const bool pos = m.ap.scale_log2 > 0.f || B_append == 0;
   const bool fp8 = kv_decode.fp8 || kv_append.fp8;   // the ABI layer allows one element type
-  const int variant = (pos ? 4 : 0) | (B_decode > 0 ? 2 : 0) | (fp8 ? 1 : 0);
+  // rotated queries come only with append-only calls (the fused rotated write)
+  if (cos_sin && B_decode > 0) return hipErrorInvalidValue;
+  const int variant = (cos_sin ? 8 : 0) | (pos ? 4 : 0) | (B_decode > 0 ? 2 : 0) | (fp8 ? 1 : 0);
   switch (variant) {
-#define RA_MIXED_CASE(V, P, D, F)                                                       \
+#define RA_MIXED_CASE(V, P, D, F, R)                                                    \
   case V:                                                                               \
-    hipLaunchKernelGGL((mixed_kernel<P, D, F>), g, b, 0, stream, m);                    \
+    hipLaunchKernelGGL((mixed_kernel<P, D, F, R>), g, b, 0, stream, m);                 \
     break;
-    RA_MIXED_CASE(0, false, false, false)
-    RA_MIXED_CASE(1, false, false, true)
-    RA_MIXED_CASE(2, false, true, false)
-    RA_MIXED_CASE(3, false, true, true)
-    RA_MIXED_CASE(4, true, false, false)
-    RA_MIXED_CASE(5, true, false, true)
-    RA_MIXED_CASE(6, true, true, false)
-    RA_MIXED_CASE(7, true, true, true)
+    RA_MIXED_CASE(0, false, false, false, false)
+    RA_MIXED_CASE(1, false, false, true, false)
+    RA_MIXED_CASE(2, false, true, false, false)
+    RA_MIXED_CASE(3, false, true, true, false)
+    RA_MIXED_CASE(4, true, false, false, false)
+    RA_MIXED_CASE(5, true, false, true, false)
+    RA_MIXED_CASE(6, true, true, false, false)
+    RA_MIXED_CASE(7, true, true, true, false)
+    RA_MIXED_CASE(8, false, false, false, true)
+    RA_MIXED_CASE(9, false, false, true, true)
+    RA_MIXED_CASE(12, true, false, false, true)
+    RA_MIXED_CASE(13, true, false, true, true)
 #undef RA_MIXED_CASE
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;

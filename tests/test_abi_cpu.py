@@ -42,7 +42,7 @@ def test_exports_every_declared_symbol(lib):
 
 def test_abi_version_and_status_strings(lib):
     declared = int(re.search(r"#define RA_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
-    assert lib.ra_abi_version() == declared == 3
+    assert lib.ra_abi_version() == declared == 4
     assert lib.ra_status_string(0) == b"RA_OK"
     assert lib.ra_status_string(4) == b"RA_ERR_WORKSPACE"
     assert lib.ra_status_string(99) == b"RA_UNKNOWN_STATUS"
@@ -342,3 +342,31 @@ def test_plain_c_caller(tmp_path):
     assert r.returncode == 0, r.stderr
     r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0 and r.stdout.strip().endswith("ok (0 failed)"), r.stdout + r.stderr
+
+
+def test_rope_validation(lib):
+    """The rotary variants check their table before anything else of theirs:
+    NULL table, no rows, or fewer rows than positions the call uses."""
+    def write(**kw):
+        d = dict(cs=FAKE, rows=64, B=2, total=4, max_new=2, max_pos=64)
+        d.update(kw)
+        return lib.kv_page_write_rope(FAKE, FAKE, FAKE, FAKE, ctypes.byref(_kv()), d["B"],
+                                      d["total"], d["max_new"], d["max_pos"], d["cs"],
+                                      d["rows"], None)
+    assert write(cs=None) == _lib.RA_ERR_NULL
+    assert write(rows=0) == _lib.RA_ERR_SHAPE
+    assert write(rows=63) == _lib.RA_ERR_SHAPE          # positions up to 63 need 64 rows
+    assert write(max_pos=65, rows=65) == _lib.RA_ERR_SHAPE   # beyond bt_stride * 16 = 64
+    assert write(B=0) == _lib.RA_OK
+
+    def fused(**kw):
+        d = dict(cs=FAKE, rows=64, max_kv=64, ws_bytes=1 << 30, total_q=10)
+        d.update(kw)
+        return lib.rollout_attn_append_write_rope(
+            FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.byref(_kv()), 2, 4, d["total_q"], 5,
+            d["max_kv"], 0.1, d["cs"], d["rows"], FAKE, None, FAKE, d["ws_bytes"], None)
+    assert fused(cs=None) == _lib.RA_ERR_NULL
+    assert fused(rows=-1) == _lib.RA_ERR_SHAPE
+    assert fused(rows=60) == _lib.RA_ERR_SHAPE          # max_kv_len 64 needs 64 rows
+    assert fused(ws_bytes=16) == _lib.RA_ERR_WORKSPACE
+    assert fused(total_q=0) == _lib.RA_OK
