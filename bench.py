@@ -436,7 +436,9 @@ def fp8_kv_leg(ra, synth, dev, wd, td, wa, ta, steps: int, warmup: int):
 
 def append_write_leg(ra, dev, wa, ta, kv_aw, kv_a, steps: int, warmup: int):
     """The append workload's page write + append as two calls and as one fused call
-    (rollout_attn_append_write), each timed alone."""
+    (rollout_attn_append_write), each timed alone; and the same with rotary
+    position embedding on write (Qwen3's table: theta 1e6), as two calls
+    (kv_page_write_rope + append) and fused (rollout_attn_append_write_rope)."""
     import torch
 
     def i32(x):
@@ -449,12 +451,21 @@ def append_write_leg(ra, dev, wa, ta, kv_aw, kv_a, steps: int, warmup: int):
     out = torch.empty((n, wa.Hq, 128), dtype=torch.float32, device=dev)
     ws = torch.empty(ra.append_workspace_size(wa.q_lens.shape[0], wa.Hq, wa.Hkv, max_q),
                      dtype=torch.uint8, device=dev)
+    inv = 1e6 ** (-2.0 * np.arange(64) / 128.0)
+    ang = np.arange(max_kv, dtype=np.float64)[:, None] * inv[None, :]
+    table = torch.from_numpy(np.concatenate([np.cos(ang), np.sin(ang)], 1).astype(np.float32))
+    table = table.to(dev)
     calls = {
         "separate": lambda: (ra.kv_page_write(k_new, v_new, cu_q, ctx, kv_aw, max_q, max_kv),
                              ra.append(ta.q_append, cu_q, ctx, kv_a, max_q, max_kv, SCALE,
                                        out=out, workspace=ws)),
         "fused": lambda: ra.append_write(ta.q_append, k_new, v_new, cu_q, ctx, kv_a, max_q,
                                          max_kv, SCALE, out=out, workspace=ws),
+        "rope_write": lambda: ra.kv_page_write(k_new, v_new, cu_q, ctx, kv_aw, max_q, max_kv,
+                                               cos_sin=table),
+        "rope_fused": lambda: ra.append_write(ta.q_append, k_new, v_new, cu_q, ctx, kv_a, max_q,
+                                              max_kv, SCALE, out=out, workspace=ws,
+                                              cos_sin=table),
     }
     ms = {}
     for name, fn in calls.items():
@@ -471,8 +482,11 @@ def append_write_leg(ra, dev, wa, ta, kv_aw, kv_a, steps: int, warmup: int):
     res = {"workload": wa.name, "steps": steps, "warmup": warmup,
            "separate_ms": round(ms["separate"], 4), "fused_ms": round(ms["fused"], 4),
            "speedup": round(ms["separate"] / ms["fused"], 4),
-           "fused_TFLOP_s": round(flops / (ms["fused"] * 1e-3) / 1e12, 1)}
-    del out, ws
+           "fused_TFLOP_s": round(flops / (ms["fused"] * 1e-3) / 1e12, 1),
+           "rope_write_ms": round(ms["rope_write"], 4),
+           "rope_fused_ms": round(ms["rope_fused"], 4),
+           "rope_fused_TFLOP_s": round(flops / (ms["rope_fused"] * 1e-3) / 1e12, 1)}
+    del out, ws, table
     return res
 
 
