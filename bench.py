@@ -737,6 +737,13 @@ def main():
         "append_write": append_write,
         "fp8_kv_decode": fp8,
         "token_logprob": logprob,
+        "paper_context": {
+            "note": "the paper's own system-level rollout throughput, on its hardware; context "
+                    "only, not comparable to the kernel metric (the paper publishes no kernel "
+                    "number)",
+            "metric": "rollout throughput, full system (Table 3)", "value": 0.37,
+            "unit": "instances/s", "hardware": "8x NVIDIA H100", "model": "Qwen3-14B",
+            "workload": "DAPO RL on SWE tasks"},
         "cpu_baseline": cpu_dec,
         "cpu_baseline_append": cpu_app,
     }
