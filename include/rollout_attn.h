@@ -41,6 +41,11 @@
  *     numbers, never an out-of-bounds access.
  *   - Results are deterministic: the same inputs give bitwise the same
  *     outputs, independent of which physical pages the block table names.
+ *   - Every entry point may be captured into a HIP graph: it allocates
+ *     nothing, never synchronizes, issues no memset or copy (work counters
+ *     are cleared by its own kernels), so each replay computes what an
+ *     eager call would. Replays of one graph must not overlap in time if
+ *     they share a workspace.
  *
  * Paged KV layout (ABI versions 2 to 4). Page size P = 16 tokens, head dim D = 128.
  * Logical token j of row b lives in physical page bt[b * bt_stride + j / P]

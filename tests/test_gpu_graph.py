@@ -1,0 +1,98 @@
+"""The library's calls under HIP graph capture (through the C ABI).
+
+Serving loops capture a whole step into a graph and replay it. Every entry
+point allocates nothing, never synchronizes and clears its own work counters
+with a kernel, so a captured step must replay to the same results as the
+eager calls, every time. The graph here holds one rollout step (page write,
+append, decode), the fused write + append and the single-launch mixed step;
+it is replayed several times with eager work and synchronizations between the
+replays, and every replay is compared bitwise with the eager results.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2603_18815_amd as ra
+import synth
+
+pytestmark = pytest.mark.gpu
+SCALE = 1.0 / math.sqrt(128)
+
+
+def i32(x, dev):
+    return torch.as_tensor(np.ascontiguousarray(np.asarray(x, np.int32)), device=dev)
+
+
+def say(msg):
+    print(f"[gpu-test] {msg}", flush=True)
+
+
+def test_step_replays_in_a_graph(device):
+    w = synth.mixed_workload(41, 24, 32, 8, 0.35,
+                             lambda r, n: synth.uniform_int(r, n, 0, 1500),
+                             lambda r, n: synth.uniform_int(r, n, 1, 300),
+                             "graph step")
+    say(f"graph: {w.decode_rows.size} decode rows, {w.append_rows.size} append rows")
+    t = synth.make_tensors(w, device)
+    kd = ra.PagedKV(t.k_pool, t.v_pool, i32(w.decode_table(), device))
+    ka = ra.PagedKV(t.k_pool, t.v_pool, i32(w.append_table(), device))
+    bt_w, cu_w, st_w = synth.write_plan(w)
+    kw = kd.with_table(i32(bt_w, device))
+    cu_w_t, st_w_t = i32(cu_w, device), i32(st_w, device)
+    lens = i32(w.kv_lens, device)
+    cu_q, ctx = i32(w.cu_q(), device), i32(w.ctx_lens, device)
+    Bd, Ba = w.kv_lens.size, w.q_lens.size
+    mk, mq = int(w.kv_lens.max()), int(w.q_lens.max())
+    mka = int((w.ctx_lens + w.q_lens).max())
+    max_new, max_pos = int(np.diff(cu_w).max()), int((np.diff(cu_w) + st_w).max())
+    nq = int(w.q_lens.sum())
+    k_chunk, v_chunk = t.k_new[-nq:], t.v_new[-nq:]
+    f32 = dict(dtype=torch.float32, device=device)
+    out_d, lse_d = torch.empty((Bd, w.Hq, 128), **f32), torch.empty((Bd, w.Hq), **f32)
+    out_a, lse_a = torch.empty((nq, w.Hq, 128), **f32), torch.empty((nq, w.Hq), **f32)
+    out_f = torch.empty((nq, w.Hq, 128), **f32)
+    out_md, out_ma = torch.empty((Bd, w.Hq, 128), **f32), torch.empty((nq, w.Hq, 128), **f32)
+    u8 = dict(dtype=torch.uint8, device=device)
+    ws_d = torch.empty(ra.decode_workspace_size(Bd, w.Hq, w.Hkv, mk), **u8)
+    ws_a = torch.empty(ra.append_workspace_size(Ba, w.Hq, w.Hkv, mq), **u8)
+    ws_f = torch.empty(ra.append_workspace_size(Ba, w.Hq, w.Hkv, mq), **u8)
+    ws_m = torch.empty(ra.mixed_workspace_size(Bd, Ba, w.Hq, w.Hkv, w.Hkv, mk, mq), **u8)
+
+    def step():
+        ra.kv_page_write(t.k_new, t.v_new, cu_w_t, st_w_t, kw, max_new, max_pos)
+        ra.append(t.q_append, cu_q, ctx, ka, mq, mka, SCALE, out=out_a, lse=lse_a,
+                  workspace=ws_a)
+        ra.decode(t.q_decode, kd, lens, mk, SCALE, out=out_d, lse=lse_d, workspace=ws_d)
+        ra.append_write(t.q_append, k_chunk, v_chunk, cu_q, ctx, ka, mq, mka, SCALE, out=out_f,
+                        workspace=ws_f)
+        ra.mixed(t.q_decode, kd, lens, t.q_append, cu_q, ctx, ka, mk, mq, mka, SCALE,
+                 out_decode=out_md, out_append=out_ma, workspace=ws_m)
+
+    outs = (out_d, lse_d, out_a, lse_a, out_f, out_md, out_ma)
+    step()                                   # eager: also brings the pools to their end state
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    pools = (t.k_pool.clone(), t.v_pool.clone())
+
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()                               # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(4):
+        for o in outs:
+            o.fill_(float("nan"))            # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, o, r in zip(("decode", "decode lse", "append", "append lse", "append_write",
+                               "mixed decode", "mixed append"), outs, ref):
+            assert torch.equal(o, r), f"replay {rep}: {name} differs from the eager result"
+        assert torch.equal(t.k_pool, pools[0]) and torch.equal(t.v_pool, pools[1])
+        say(f"graph replay {rep}: bitwise equal to eager")
