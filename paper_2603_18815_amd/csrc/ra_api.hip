@@ -78,7 +78,7 @@ int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_
   if (s != RA_OK) return s;
   if (!q || !kv_lens || !out) return RA_ERR_NULL;
   if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
-  if (Hq / kv->num_kv_heads > 16 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (Hq / kv->num_kv_heads > 32 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
   if (!positions_fit(kv, max_kv_len)) return RA_ERR_SHAPE;
   if (B == 0) return RA_OK;
   const ra::DecodePlan plan = ra::decode_plan(B, kv->num_kv_heads, max_kv_len);

@@ -74,7 +74,12 @@ hipError_t launch_decode(const uint16_t *q, const PagedKV &kv, const int32_t *kv
                          void *workspace, const DecodePlan &plan, hipStream_t stream) {
   const DecodeArgs a =
       make_decode_args(q, kv, kv_lens, B, hq, max_kv_len, scale, workspace, plan.max_splits, plan);
-  launch_split<1, false>(kv.fp8, dim3(kv.hkv, plan.max_splits, B), a, stream);
+  // the G query heads of a KV head are the columns of one 16-column tile, or
+  // of two for groups of 17 to 32 heads
+  if (a.group > 16)
+    launch_split<2, false>(kv.fp8, dim3(kv.hkv, plan.max_splits, B), a, stream);
+  else
+    launch_split<1, false>(kv.fp8, dim3(kv.hkv, plan.max_splits, B), a, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(hq, B), dim3(kHeadDim), 0, stream, a, out, lse);

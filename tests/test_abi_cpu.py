@@ -75,7 +75,8 @@ def test_decode_validation(lib):
     assert _decode(lib, _kv(), max_kv_len=65) == _lib.RA_ERR_SHAPE        # > bt_stride * 16
     assert _decode(lib, _kv(page_size=32)) == _lib.RA_ERR_UNSUPPORTED
     assert _decode(lib, _kv(head_dim=64)) == _lib.RA_ERR_UNSUPPORTED
-    assert _decode(lib, _kv(), Hq=34) == _lib.RA_ERR_UNSUPPORTED          # group of 17
+    assert _decode(lib, _kv(), Hq=66) == _lib.RA_ERR_UNSUPPORTED          # group of 33
+    assert _decode(lib, _kv(), Hq=64, B=0) == _lib.RA_OK                  # group of 32
     assert _decode(lib, _kv(), ws_bytes=16) == _lib.RA_ERR_WORKSPACE
     assert _decode(lib, _kv(), ws=None) == _lib.RA_ERR_WORKSPACE
     assert _decode(lib, _kv(), B=0) == _lib.RA_OK                         # no work, no launch

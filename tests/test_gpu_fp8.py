@@ -75,7 +75,7 @@ def test_fp8_page_write_every_bf16_value_bitexact(device, k_scale, v_scale):
     assert (q == 0x7F).any() and ((q == 0x7E) | (q == 0xFE)).any()   # NaN and saturation seen
 
 
-@pytest.mark.parametrize("Hq,Hkv", [(32, 8), (8, 8), (16, 1), (8, 2)])
+@pytest.mark.parametrize("Hq,Hkv", [(32, 8), (8, 8), (16, 1), (8, 2), (32, 1)])
 def test_fp8_decode_vs_oracle(device, Hq, Hkv):
     lens = [1, 15, 16, 17, 31, 32, 33, 300, 1000, 2049, 4100]
     ks, vs = 2.0 ** -5, 0.0625

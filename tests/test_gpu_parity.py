@@ -131,7 +131,7 @@ def test_decode_parity_full_size_sampled_rows(device, c):
                                atol=1e-4, rtol=0)
 
 
-@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (4, 2), (32, 8), (64, 8), (32, 2)])
+@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (4, 2), (32, 8), (64, 8), (32, 2), (24, 1), (32, 1)])
 def test_decode_edge_lengths_and_groups(device, Hq, Hkv):
     lens = [1, 2, 15, 16, 17, 31, 32, 33, 127, 128, 129, 300, 1000]
     say(f"decode edges Hq={Hq} Hkv={Hkv}")
