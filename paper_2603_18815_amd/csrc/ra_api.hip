@@ -111,7 +111,7 @@ int rollout_attn_decode_shared_prefix(const void *q, const ra_paged_kv *kv,
   if (s != RA_OK) return s;
   if (!q || !kv_lens || !out || !group_start || !prefix_len) return RA_ERR_NULL;
   if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
-  if (Hq / kv->num_kv_heads > 16 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (Hq / kv->num_kv_heads > 32 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
   if (!positions_fit(kv, max_kv_len) || max_prefix_len > max_kv_len) return RA_ERR_SHAPE;
   if (B == 0) return RA_OK;
   if (num_groups == 0 || max_group_rows == 0 || max_group_rows > B || num_groups > B)

@@ -122,7 +122,11 @@ hipError_t launch_decode_shared_prefix(const uint16_t *q, const PagedKV &kv,
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   a.zdiv = max_group_rows;
-  launch_split<1, false>(kv.fp8, dim3(kv.hkv, plan.max_splits, (unsigned)sh.row_z), a, stream);
+  const dim3 rows_grid(kv.hkv, plan.max_splits, (unsigned)sh.row_z);
+  if (a.group > 16)
+    launch_split<2, false>(kv.fp8, rows_grid, a, stream);
+  else
+    launch_split<1, false>(kv.fp8, rows_grid, a, stream);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(hq, (unsigned)sh.row_z), dim3(kHeadDim), 0, stream,
                      a, out, lse);

@@ -99,7 +99,7 @@ def test_shared_prefix_decode_validation(lib):
     assert call(mgr=17) == _lib.RA_ERR_SHAPE         # more rows per group than rows
     assert call(mpl=65) == _lib.RA_ERR_SHAPE         # prefix bound above max_kv_len
     assert call(Hq=5) == _lib.RA_ERR_SHAPE
-    assert call(Hq=34) == _lib.RA_ERR_UNSUPPORTED    # group of 17 query heads
+    assert call(Hq=66) == _lib.RA_ERR_UNSUPPORTED    # group of 33 query heads
     assert call(ws_bytes=16) == _lib.RA_ERR_WORKSPACE
     assert call(ws=None) == _lib.RA_ERR_WORKSPACE
     big = dict(B=65535, ng=65535, mgr=2, max_kv_len=64)
