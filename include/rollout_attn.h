@@ -92,8 +92,8 @@ typedef enum {
   RA_ERR_NULL = 1,        /* a required pointer is NULL */
   RA_ERR_SHAPE = 2,       /* inconsistent sizes (negative, Hq % Hkv != 0, ...) */
   RA_ERR_UNSUPPORTED = 3, /* valid but not built: page_size != 16, head_dim != 128,
-                             a group size Hq / Hkv above 32 (decode,
-                             shared-prefix decode) or 16 (mixed), an unknown kv_dtype,
+                             a decode group size Hq / Hkv above 32, an
+                             unknown kv_dtype,
                              pools of two element types in one mixed call */
   RA_ERR_WORKSPACE = 4,   /* workspace smaller than the *_workspace_size value */
   RA_ERR_HIP = 5          /* a HIP launch failed (no device, bad stream, ...) */

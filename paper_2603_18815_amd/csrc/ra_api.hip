@@ -283,7 +283,7 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
     if ((s = check_kv(kv_decode)) != RA_OK) return s;
     if (!q_decode || !kv_lens || !out_decode) return RA_ERR_NULL;
     if (Hq % kv_decode->num_kv_heads != 0) return RA_ERR_SHAPE;
-    if (Hq / kv_decode->num_kv_heads > 16 || B_decode > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+    if (Hq / kv_decode->num_kv_heads > 32 || B_decode > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
     if (!positions_fit(kv_decode, max_kv_len_decode)) return RA_ERR_SHAPE;
   }
   if (app) {

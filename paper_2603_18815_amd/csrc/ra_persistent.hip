@@ -230,12 +230,13 @@ __global__ __launch_bounds__(kPlanThreads) void mixed_plan_kernel(MixedArgs m, p
 
 // kDecode: the call has decode rows (otherwise every entry is an append tile).
 // kFp8: the pools hold E4M3 codes. kRope: the append rows' q is rotated at its
-// position (append-only calls).
-template <bool kPosScale, bool kDecode, bool kFp8, bool kRope = false>
+// position (append-only calls). kDecodeTiles: 16-column tiles of a decode
+// split (2 for groups of 17 to 32 query heads).
+template <bool kPosScale, bool kDecode, bool kFp8, bool kRope = false, int kDecodeTiles = 1>
 __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
   __shared__ union {
     atile::AppendLds ap;
-    dsplit::DecodeLds<1, kMixWaves> de;
+    dsplit::DecodeLds<kDecodeTiles, kMixWaves> de;
   } lds;
   __shared__ int s_next;
   // workgroups are placed on the XCDs round robin: start with this XCD's
@@ -256,7 +257,8 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
       const int dj = (int)((int64_t)j * nd / n);
       if (kDecode && (int)(((int64_t)j + 1) * nd / n) > dj) {
         const int2 e = splits[dj];
-        dsplit::decode_split<1, false, kMixWaves, kFp8>(m.de, e.y & ((1 << kHeadBits) - 1),
+        dsplit::decode_split<kDecodeTiles, false, kMixWaves, kFp8>(m.de,
+                                                                   e.y & ((1 << kHeadBits) - 1),
                                                         e.y >> kHeadBits, e.x, lds.de);
       } else {
         const int2 e = tiles[j - dj];
@@ -339,25 +341,33 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   const bool fp8 = kv_decode.fp8 || kv_append.fp8;   // the ABI layer allows one element type
   // rotated queries come only with append-only calls (the fused rotated write)
   if (cos_sin && B_decode > 0) return hipErrorInvalidValue;
-  const int variant = (cos_sin ? 8 : 0) | (pos ? 4 : 0) | (B_decode > 0 ? 2 : 0) | (fp8 ? 1 : 0);
-  switch (variant) {
+  if (B_decode > 0 && m.de.group > 16) {   // two-tile decode splits
+    const int v2 = (pos ? 2 : 0) | (fp8 ? 1 : 0);
+    if (v2 == 0) hipLaunchKernelGGL((mixed_kernel<false, true, false, false, 2>), g, b, 0, stream, m);
+    if (v2 == 1) hipLaunchKernelGGL((mixed_kernel<false, true, true, false, 2>), g, b, 0, stream, m);
+    if (v2 == 2) hipLaunchKernelGGL((mixed_kernel<true, true, false, false, 2>), g, b, 0, stream, m);
+    if (v2 == 3) hipLaunchKernelGGL((mixed_kernel<true, true, true, false, 2>), g, b, 0, stream, m);
+  } else {
+    const int variant = (cos_sin ? 8 : 0) | (pos ? 4 : 0) | (B_decode > 0 ? 2 : 0) | (fp8 ? 1 : 0);
+    switch (variant) {
 #define RA_MIXED_CASE(V, P, D, F, R)                                                    \
-  case V:                                                                               \
-    hipLaunchKernelGGL((mixed_kernel<P, D, F, R>), g, b, 0, stream, m);                 \
-    break;
-    RA_MIXED_CASE(0, false, false, false, false)
-    RA_MIXED_CASE(1, false, false, true, false)
-    RA_MIXED_CASE(2, false, true, false, false)
-    RA_MIXED_CASE(3, false, true, true, false)
-    RA_MIXED_CASE(4, true, false, false, false)
-    RA_MIXED_CASE(5, true, false, true, false)
-    RA_MIXED_CASE(6, true, true, false, false)
-    RA_MIXED_CASE(7, true, true, true, false)
-    RA_MIXED_CASE(8, false, false, false, true)
-    RA_MIXED_CASE(9, false, false, true, true)
-    RA_MIXED_CASE(12, true, false, false, true)
-    RA_MIXED_CASE(13, true, false, true, true)
+    case V:                                                                               \
+      hipLaunchKernelGGL((mixed_kernel<P, D, F, R>), g, b, 0, stream, m);                 \
+      break;
+      RA_MIXED_CASE(0, false, false, false, false)
+      RA_MIXED_CASE(1, false, false, true, false)
+      RA_MIXED_CASE(2, false, true, false, false)
+      RA_MIXED_CASE(3, false, true, true, false)
+      RA_MIXED_CASE(4, true, false, false, false)
+      RA_MIXED_CASE(5, true, false, true, false)
+      RA_MIXED_CASE(6, true, true, false, false)
+      RA_MIXED_CASE(7, true, true, true, false)
+      RA_MIXED_CASE(8, false, false, false, true)
+      RA_MIXED_CASE(9, false, false, true, true)
+      RA_MIXED_CASE(12, true, false, false, true)
+      RA_MIXED_CASE(13, true, false, true, true)
 #undef RA_MIXED_CASE
+    }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (B_decode == 0) return hipSuccess;

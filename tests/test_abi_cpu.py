@@ -247,7 +247,7 @@ def test_mixed_validation(lib):
     assert _mixed(lib, kv, kv, Hq=3) == _lib.RA_ERR_SHAPE                # Hq % Hkv
     assert _mixed(lib, kv, kv, mkd=65) == _lib.RA_ERR_SHAPE              # > bt_stride * 16
     assert _mixed(lib, kv, kv, mq=65, mka=64) == _lib.RA_ERR_SHAPE       # chunk > max_kv_len
-    assert _mixed(lib, kv, kv, Hq=34) == _lib.RA_ERR_UNSUPPORTED         # decode group of 17
+    assert _mixed(lib, kv, kv, Hq=66) == _lib.RA_ERR_UNSUPPORTED         # decode group of 33
     assert _mixed(lib, kv, _kv(page_size=32)) == _lib.RA_ERR_UNSUPPORTED
     assert _mixed(lib, kv, _kv(num_kv_heads=512, num_pages=10), Hq=512,
                   Bd=0) == _lib.RA_ERR_UNSUPPORTED                       # > 256 KV heads

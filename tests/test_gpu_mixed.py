@@ -52,7 +52,7 @@ def run_mixed(w, t, dev, kv_lens=None, **kw):
                     want_lse=True, **kw)
 
 
-@pytest.mark.parametrize("Hq,Hkv", [(32, 8), (8, 8), (16, 1), (64, 8)])
+@pytest.mark.parametrize("Hq,Hkv", [(32, 8), (8, 8), (16, 1), (64, 8), (32, 1)])
 def test_mixed_small_vs_oracle_and_separate_calls(device, Hq, Hkv):
     w = small_mixed(Hq + Hkv, 24, Hq, Hkv)
     say(f"mixed {w.name}: {w.decode_rows.size} decode rows, {w.append_rows.size} append rows")
