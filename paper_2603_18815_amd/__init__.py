@@ -37,6 +37,9 @@ def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
 
 
 def _need(t: torch.Tensor, name: str, dtype: torch.dtype, device: torch.device) -> None:
+    # the kernels dereference every pointer on the GPU: host tensors are refused
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor, got one on {t.device}")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
     if t.device != device:
