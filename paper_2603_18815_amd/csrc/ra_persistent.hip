@@ -350,10 +350,10 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   } else {
     const int variant = (cos_sin ? 8 : 0) | (pos ? 4 : 0) | (B_decode > 0 ? 2 : 0) | (fp8 ? 1 : 0);
     switch (variant) {
-#define RA_MIXED_CASE(V, P, D, F, R)                                                    \
-    case V:                                                                               \
-      hipLaunchKernelGGL((mixed_kernel<P, D, F, R>), g, b, 0, stream, m);                 \
-      break;
+#define RA_MIXED_CASE(V, P, D, F, R)                                                  \
+  case V:                                                                             \
+    hipLaunchKernelGGL((mixed_kernel<P, D, F, R>), g, b, 0, stream, m);               \
+    break;
       RA_MIXED_CASE(0, false, false, false, false)
       RA_MIXED_CASE(1, false, false, true, false)
       RA_MIXED_CASE(2, false, true, false, false)
