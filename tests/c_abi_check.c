@@ -90,6 +90,20 @@ int main(void) {
          RA_ERR_NULL);
   expect("page write: max_pos past the table",
          kv_page_write(fake, fake, ifake, ifake, &kv, 2, 4, 2, 65, 0), RA_ERR_SHAPE);
+  expect("page write rope: NULL table",
+         kv_page_write_rope(fake, fake, ifake, ifake, &kv, 2, 4, 2, 32, NULL, 64, 0),
+         RA_ERR_NULL);
+  expect("page write rope: table shorter than max_pos",
+         kv_page_write_rope(fake, fake, ifake, ifake, &kv, 2, 4, 2, 32, ffake, 31, 0),
+         RA_ERR_SHAPE);
+  expect("append_write rope: no table rows",
+         rollout_attn_append_write_rope(fake, fake, fake, ifake, ifake, &kv, 2, 4, 10, 5, 64,
+                                        0.1f, ffake, 0, ffake, NULL, ws, sizeof ws, 0),
+         RA_ERR_SHAPE);
+  expect("append_write rope: small workspace",
+         rollout_attn_append_write_rope(fake, fake, fake, ifake, ifake, &kv, 2, 4, 10, 5, 64,
+                                        0.1f, ffake, 64, ffake, NULL, ws, sizeof ws, 0),
+         RA_ERR_WORKSPACE);
   expect("page gather: NULL k_out",
          kv_page_gather(&kv, ifake, ifake, 2, 8, 4, NULL, fake, 0), RA_ERR_NULL);
   kv.kv_dtype = RA_KV_FP8_E4M3;
