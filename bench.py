@@ -563,7 +563,7 @@ def main():
                          "'logprob' the LM-head log-probability leg); prints no JSON line")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
               "(rows shard by trajectory with no exchange; see the design notes).",
               file=sys.stderr)
         sys.exit(2)
