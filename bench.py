@@ -557,12 +557,12 @@ def main():
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-step leg (B = 512, 85 %% decode / 15 %% append rows)")
     ap.add_argument("--only", choices=["write", "decode", "append", "copy", "mixed", "logprob",
-                                       "decode_fp8"],
+                                       "decode_fp8", "append_fp8"],
                     help="run only this part of the step --steps times after --warmup "
                          "(for rocprofv3 runs; 'copy' is a 1 GiB torch copy used to "
                          "calibrate the HBM byte counters, 'mixed' the mixed-step leg, "
-                         "'logprob' the LM-head log-probability leg, 'decode_fp8' the decode "
-                         "workload over fp8 pools); prints no JSON line")
+                         "'logprob' the LM-head log-probability leg, 'decode_fp8' / 'append_fp8' "
+                         "the decode / append workload over fp8 pools); prints no JSON line")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path "
@@ -643,6 +643,16 @@ def main():
                              i32(wd.decode_table()), ks, vs)
             part = lambda: ra.decode(td.q_decode, kv8, kv_lens, max_kv_d, SCALE, out=out_d,
                                      workspace=ws)
+        elif args.only == "append_fp8":
+            # fp8 pools for the append workload's rows (scales as in the fp8 leg)
+            ks = vs = 2.0 ** -5
+            gen = synth.value_generator(1235, dev)
+            n = wa.layout.num_pages
+            kva8 = ra.PagedKV(synth.randn_fp8_codes((n, wa.Hkv, 16, 128), gen, dev, ks),
+                              synth.randn_fp8_codes((n, wa.Hkv, 128, 16), gen, dev, vs),
+                              i32(wa.append_table()), ks, vs)
+            part = lambda: ra.append(ta.q_append, cu_q, ctx, kva8, max_q, max_kv_a, SCALE,
+                                     out=out_a, workspace=ws_a)
         else:
             part = {"write": lambda: (ra.kv_page_write(td.k_new, td.v_new, cu_d_t, st_d_t, kv_dw,
                                                        max_new_d, max_pos_d),
