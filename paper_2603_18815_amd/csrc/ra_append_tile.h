@@ -7,11 +7,14 @@
 // "query rows" (query, head), 32 per wave, each wave's rows forming the 32
 // columns of its 32x32 matrix tiles with their Q^T operands in registers.
 // The key loop walks the row's pages 64 keys (4 pages) at a time. Each block
-// of K and V is loaded once per workgroup into registers, stored to one of
-// two LDS buffers (the load of the next block is in flight while the current
-// one is used), one barrier per block, and all eight waves consume it:
+// of K and V is loaded once per workgroup into registers and stored to a ring
+// of four LDS buffers, one barrier per block, and all eight waves consume it:
 //   S^T[key][qrow] = K[key][:] · Q^T[:][qrow]        (bf16 mfma 32x32x16, fp32)
 //   O^T[d][qrow]  += V^T[d][key] · P^T[key][qrow]    (P rounded to bf16)
+// The work is software-pipelined over pairs of pages (32 keys): the step that
+// takes the softmax of pair p also issues the P·V products of pair p - 1 and
+// the score products of pair p + 1, none of which depends on that softmax, so
+// the matrix cores are kept busy by the same wave while it exponentiates.
 // Keys are ordered inside each pair of pages so that the 16 S values a lane
 // receives are, in order, 8 consecutive slots of the first page and the same
 // 8 slots of the second: exactly the P^T operands of the two P·V products it
@@ -23,6 +26,8 @@
 // ctx + i) is applied only on blocks that reach past the wave's first query
 // position.
 #pragma once
+
+#include <type_traits>
 
 #include "ra_device.h"
 #include "ra_internal.h"
@@ -93,10 +98,11 @@ __device__ __forceinline__ int v_lds(int page, int d, int half) {
   return (page * kHeadDim + d) * kPage + ((half ^ ((d >> 3) & 1)) * 8);
 }
 
-// LDS of one tile: double-buffered K and V blocks.
+// LDS of one tile: a ring of four K and V blocks (block B in buffer B % 4).
+constexpr int kBuffers = 4;
 struct AppendLds {
-  __attribute__((aligned(16))) uint16_t k[2 * kKBlockElems];
-  __attribute__((aligned(16))) uint16_t v[2 * kBlockElems];
+  __attribute__((aligned(16))) uint16_t k[kBuffers * kKBlockElems];
+  __attribute__((aligned(16))) uint16_t v[kBuffers * kBlockElems];
 };
 
 // Row b's chunk: its first query in q / out (cu0), its length T and the
@@ -273,111 +279,133 @@ __device__ __forceinline__ void append_tile(const AppendArgs &a, int qblk, int g
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;   // running max (scaled, base 2) and sum
 
+  // S^T of pair pp of the block in LDS buffer buf: 32 keys x 32 query rows.
+  auto scores = [&](int buf, int pp) __attribute__((always_inline)) {
+    const uint16_t *kl = sK + buf * kKBlockElems;
+    const int krow = 32 * pp + ka_key;
+    f32x16 st = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk)
+      st = mfma32x32x16(lds_bf16x8(&kl[k_lds(krow, 2 * kk + grp)]), qop[kk], st);
+    return st;
+  };
+
+  // Software pipeline over pairs of pages (32 keys). Step p computes the
+  // softmax of pair p while the matrix cores run P·V of pair p - 1 and the
+  // scores of pair p + 1, none of which depends on it. Blocks of 64 keys
+  // rotate through four LDS buffers: while block B is computed, block B - 1
+  // is still read (V of its last pair), block B + 1 is complete (keys of the
+  // look-ahead scores) and block B + 2 is being stored. Block -1 (the last
+  // buffer) holds zero V operands (its second pair) for the first step's P·V,
+  // whose weights are zero too.
+  static_assert(kThreads * 8 == kBlockElems / 2, "one 16-byte store per thread");
+  *reinterpret_cast<u32x4 *>(&sV[(kBuffers - 1) * kBlockElems + kBlockElems / 2 + 8 * tid]) =
+      u32x4{};
   stage_load(0);
   stage_store(0, 0);
-  __syncthreads();
-
-  for (int blk = 0; blk < nblocks; ++blk) {
-    const int buf = blk & 1;
-    if (blk + 1 < nblocks) stage_load(blk + 1);
-    const uint16_t *kl = sK + buf * kKBlockElems;
-    const uint16_t *vl = sV + buf * kBlockElems;
-    const int key0 = blk * kBlock;
-    const bool need_mask = key0 + kBlock - 1 > wave_q0;
-
-    // S^T of pair pp: 32 keys (pages 2pp, 2pp + 1 of the block) x 32 query rows.
-    auto scores = [&](int pp) __attribute__((always_inline)) {
-      // all eight K operands are requested before the first product
-      const int krow = 32 * pp + ka_key;
-      bf16x8 ka[8];
-#pragma unroll
-      for (int kk = 0; kk < 8; ++kk) ka[kk] = lds_bf16x8(&kl[k_lds(krow, 2 * kk + grp)]);
-      f32x16 st = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < 8; ++kk) st = mfma32x32x16(ka[kk], qop[kk], st);
-      return st;
-    };
-    // Online-softmax update and P·V of pair pp.
-    auto update = [&](int pp, f32x16 st) __attribute__((always_inline)) {
-      // V operands are requested first; their latency hides behind the softmax.
-      bf16x8 va[8];
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        va[2 * dt] = lds_bf16x8(&vl[v_lds(2 * pp, 32 * dt + col, grp)]);
-        va[2 * dt + 1] = lds_bf16x8(&vl[v_lds(2 * pp + 1, 32 * dt + col, grp)]);
-      }
-      float sc[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sc[r] = kPosScale ? st[r] : st[r] * c2;
-      if (need_mask) {
-        // value r is key key0 + 32 pp + 8 grp + 16 (r / 8) + r % 8; masked past qpos
-        const int rel = qpos - key0 - 32 * pp - 8 * grp;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sc[r] = 16 * (r >> 3) + (r & 7) > rel ? -INFINITY : sc[r];
-      }
-      // Weights against the running max m_run. It is only moved (and O, l
-      // rescaled) when some lane's weights sum past kSumLimit, or are not
-      // finite (the first pair, while m_run is still -inf); the weights are
-      // then recomputed against the new max. Between moves every weight
-      // stays below kSumLimit, which fp32 and bf16 carry without loss, and
-      // out = O / l does not depend on when the max moves.
-      f32x8 p0, p1;
-      bf16x8 pb0, pb1;
-      float psum;
-      // Weights, rounded to bf16 for the P·V product, and their sum taken
-      // from the rounded values (two chains of bf16 pair dot products with
-      // (1, 1)), so that l normalises exactly the weights O accumulates.
-      auto weights = [&]() __attribute__((always_inline)) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          p0[e] = fast_exp2(__builtin_fmaf(sc[e], cs, -m_run));
-          p1[e] = fast_exp2(__builtin_fmaf(sc[8 + e], cs, -m_run));
-        }
-        pb0 = to_bf16x8(p0);
-        pb1 = to_bf16x8(p1);
-        const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
-        float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          s0 = __builtin_amdgcn_fdot2_f32_bf16(
-              bf16x2{pb0[2 * e], pb0[2 * e + 1]}, one, s0, false);
-          s1 = __builtin_amdgcn_fdot2_f32_bf16(
-              bf16x2{pb1[2 * e], pb1[2 * e + 1]}, one, s1, false);
-        }
-        psum = s0 + s1;
-      };
-      weights();
-      if (!__all(psum <= kSumLimit)) {
-        float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
-#pragma unroll
-        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
-        mx = fmaxf(mx, sc[15]);
-        mx = pair_max(mx);
-        if (kPosScale) mx *= c2;
-        float m_new = fmaxf(m_run, mx);
-        if (m_new == -INFINITY) m_new = 0.f;   // nothing attended yet: any finite reference
-        const float alpha = fast_exp2(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
-        weights();
-      }
-      l_run += psum;
-      // O^T[d][qrow] += V^T[d][key] P^T[key][qrow]: page c of the pair, slots
-      // 8 grp + 0..7, d = 32 dt + col.
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        o[dt] = mfma32x32x16(va[2 * dt], pb0, o[dt]);
-        o[dt] = mfma32x32x16(va[2 * dt + 1], pb1, o[dt]);
-      }
-    };
-#pragma unroll
-    for (int pp = 0; pp < kBlock / 32; ++pp) update(pp, scores(pp));
-
-    if (blk + 1 < nblocks) stage_store(blk + 1, buf ^ 1);
-    __syncthreads();
+  if (nblocks > 1) {
+    stage_load(1);
+    stage_store(1, 1);
   }
+  __syncthreads();
+  f32x16 st = scores(0, 0);
+  bf16x8 pb0 = bf16x8{}, pb1 = bf16x8{};   // weights of the previous pair (none yet)
+
+  // P·V of pair pp of the block in buffer buf, weights pb0, pb1:
+  // O^T[d][qrow] += V^T[d][key] P^T[key][qrow], page c of the pair, slots
+  // 8 grp + 0..7, d = 32 dt + col
+  auto pv = [&](int buf, int pp) __attribute__((always_inline)) {
+    const uint16_t *vl = sV + buf * kBlockElems;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      o[dt] = mfma32x32x16(lds_bf16x8(&vl[v_lds(2 * pp, 32 * dt + col, grp)]), pb0, o[dt]);
+      o[dt] = mfma32x32x16(lds_bf16x8(&vl[v_lds(2 * pp + 1, 32 * dt + col, grp)]), pb1, o[dt]);
+    }
+  };
+
+  // One step: pair pp of the block starting at key key0. (vbuf, vpp): the
+  // previous pair, whose P·V is issued now; (kbuf, kpp): the next pair, whose
+  // scores are computed now. mask_tag: the block reaches past the wave's
+  // first query (causal mask on).
+  auto step = [&](int vbuf, int vpp, int kbuf, int kpp, int pp, int key0, auto mask_tag)
+      __attribute__((always_inline)) {
+    constexpr bool kMask = decltype(mask_tag)::value;
+    pv(vbuf, vpp);   // the previous pair
+    // scores of the next pair
+    const f32x16 st_next = scores(kbuf, kpp);
+
+    float sc[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc[r] = kPosScale ? st[r] : st[r] * c2;
+    if constexpr (kMask) {
+      // value r is key key0 + 32 pp + 8 grp + 16 (r / 8) + r % 8; masked past qpos
+      const int rel = qpos - key0 - 32 * pp - 8 * grp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[r] = 16 * (r >> 3) + (r & 7) > rel ? -INFINITY : sc[r];
+    }
+    // Weights against the running max m_run. It is only moved (and O, l
+    // rescaled) when some lane's weights sum past kSumLimit, or are not
+    // finite (the first pair, while m_run is still -inf); the weights are
+    // then recomputed against the new max. Between moves every weight
+    // stays below kSumLimit, which fp32 and bf16 carry without loss, and
+    // out = O / l does not depend on when the max moves.
+    float psum;
+    auto weights = [&]() __attribute__((always_inline)) {
+      f32x8 p0, p1;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p0[e] = fast_exp2(__builtin_fmaf(sc[e], cs, -m_run));
+        p1[e] = fast_exp2(__builtin_fmaf(sc[8 + e], cs, -m_run));
+      }
+      pb0 = to_bf16x8(p0);
+      pb1 = to_bf16x8(p1);
+      const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+      float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb0[2 * e], pb0[2 * e + 1]}, one, s0, false);
+        s1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb1[2 * e], pb1[2 * e + 1]}, one, s1, false);
+      }
+      psum = s0 + s1;
+    };
+    weights();
+    if (!__all(psum <= kSumLimit)) {
+      float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+#pragma unroll
+      for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
+      mx = fmaxf(mx, sc[15]);
+      mx = pair_max(mx);
+      if (kPosScale) mx *= c2;
+      float m_new = fmaxf(m_run, mx);
+      if (m_new == -INFINITY) m_new = 0.f;   // nothing attended yet: any finite reference
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
+      weights();
+    }
+    l_run += psum;
+    st = st_next;
+  };
+
+  auto block = [&](int blk, auto mask_tag) __attribute__((always_inline)) {
+    const int bcur = blk % kBuffers, bprev = (blk + kBuffers - 1) % kBuffers,
+              bnext = (blk + 1) % kBuffers;
+    if (blk + 2 < nblocks) stage_load(blk + 2);
+    const int key0 = blk * kBlock;
+    step(bprev, 1, bcur, 1, 0, key0, mask_tag);
+    step(bcur, 0, bnext, 0, 1, key0, mask_tag);
+    if (blk + 2 < nblocks) stage_store(blk + 2, (blk + 2) % kBuffers);
+    __syncthreads();
+  };
+  // Blocks from mb on reach past the wave's first query and take the causal
+  // mask; every wave passes the same barriers (one per block).
+  const int mb = __builtin_amdgcn_readfirstlane(min(nblocks, (wave_q0 + 1) / kBlock));
+  int blk = 0;
+  for (; blk < mb; ++blk) block(blk, std::false_type{});
+  for (; blk < nblocks; ++blk) block(blk, std::true_type{});
+  pv((nblocks - 1) % kBuffers, 1);   // the last pair
 
   // ---- epilogue: normalise and store; lane holds d = 32 dt + 8 (r/4) + 4 grp + r%4 ----
   const float l = l_run + __shfl_xor(l_run, 32);
