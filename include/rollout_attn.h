@@ -396,33 +396,55 @@ int token_logprob_packed(const void *h, const void *W_packed, const int32_t *tar
                          void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
- * Page write: scatter new tokens' keys and values into their pages, a bit
- * copy into bf16 pools, a quantization into fp8 pools (each element stored as
- * encode(fp32(x) * fp32(1 / scale)), see the layout above). Row b's new
- * tokens are packed rows cu_new[b] .. cu_new[b+1]-1 of k_new / v_new; token t
- * of the row goes to logical position start_pos[b] + t. No other pool byte
- * changes. Rows of one call must not write the same slot.
+ * Page write: append new tokens' keys and values to each trajectory's cache
+ * (Sec. 3.3.3: the tokens of earlier turns are kept as they are and only the
+ * new observation tokens are tokenised and added after them; Sec. 3.3.2: each
+ * agent step's completion extends the same history, so every decoded token is
+ * added too). The cache that later steps reuse (Sec. 3.3.2, load balancing
+ * keeps a task on one backend for this) is therefore only ever extended at
+ * its end, one chunk or one token per row and call.
+ * The write is a bit copy into bf16 pools and a quantization into fp8 pools
+ * (each element stored as encode(fp32(x) * fp32(1 / scale)), see the layout
+ * above). Row b's new tokens are packed rows cu_new[b] .. cu_new[b+1]-1 of
+ * k_new / v_new; token t of the row goes to logical position start_pos[b] + t,
+ * i.e. page bt[b][(start_pos[b] + t) / 16], slot (start_pos[b] + t) % 16. No
+ * other pool byte changes. Rows of one call must not write the same slot.
  *
- *   k_new, v_new  bf16 [total_new][Hkv][128] (token-major)
- *   cu_new        int32 [B+1]
+ *   k_new, v_new  bf16 [total_new][Hkv][128] (token-major), read only
+ *   cu_new        int32 [B+1], non-decreasing, cu_new[0] = 0
  *   start_pos     int32 [B]
+ *   kv            pools written in place (caller-owned), block table read
+ *   B, total_new  host: rows and packed tokens of the call
  *   max_new       host: an upper bound of cu_new[b+1] - cu_new[b]
  *   max_pos       host: an upper bound of start_pos[b] + new tokens of row b;
  *                 <= bt_stride * 16
+ * Errors: RA_ERR_NULL (a NULL pointer), RA_ERR_SHAPE (negative sizes,
+ *         max_pos > bt_stride * 16, max_new > max_pos, bad fp8 scales),
+ *         RA_ERR_UNSUPPORTED (page_size != 16, head_dim != 128, B > 65535),
+ *         RA_ERR_HIP. B == 0, total_new == 0 or max_new == 0 launch nothing.
  */
 int kv_page_write(const void *k_new, const void *v_new, const int32_t *cu_new,
                   const int32_t *start_pos, const ra_paged_kv *kv, int32_t B, int32_t total_new,
                   int32_t max_new, int32_t max_pos, hipStream_t stream);
 
 /*
- * Page gather (test and export helper): copy logical tokens 0 .. lens[b]-1 of
- * every row out of the pages into packed token-major arrays; row b starts at
- * packed row cu_out[b]. A bit copy of the stored elements (E4M3 codes for fp8
- * pools).
+ * Page gather (test and export helper): read back, in logical order, the
+ * cached history of each trajectory that the attention entry points attend to
+ * (Sec. 3.3.2: a task's later calls reuse its cached prefix; Sec. 3.3.3: that
+ * prefix is the retained token sequence with the observations appended). It
+ * copies logical tokens 0 .. lens[b]-1 of every row out of the pages (token j
+ * from page bt[b][j / 16], slot j % 16) into packed token-major arrays; row b
+ * starts at packed row cu_out[b]. A bit copy of the stored elements (E4M3
+ * codes for fp8 pools); it checks a write and exports a trajectory's cache.
  *
+ *   kv       pools and block table, read only
  *   lens     int32 [B]; max_len host upper bound of lens (<= bt_stride * 16)
- *   cu_out   int32 [B+1]
- *   k_out, v_out  [total][Hkv][128] of the pools' element type
+ *   cu_out   int32 [B+1], non-decreasing, cu_out[0] = 0, cu_out[B] <= total
+ *   k_out, v_out  [total][Hkv][128] of the pools' element type (caller-owned,
+ *            written)
+ * Errors: RA_ERR_NULL, RA_ERR_SHAPE (negative sizes, max_len > bt_stride *
+ *         16), RA_ERR_UNSUPPORTED (B > 65535, unsupported page layout),
+ *         RA_ERR_HIP. B == 0, total == 0 or max_len == 0 launch nothing.
  */
 int kv_page_gather(const ra_paged_kv *kv, const int32_t *lens, const int32_t *cu_out, int32_t B,
                    int32_t total, int32_t max_len, void *k_out, void *v_out,

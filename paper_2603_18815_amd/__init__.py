@@ -6,6 +6,14 @@ device pointers plus torch's current HIP stream to the library; every step of
 the computation runs in the library's HIP kernels. If the library is not built
 the import of any function fails loudly: there is no fallback path.
 
+Host-side sizes (max_kv_len, max_q_len, max_new, max_pos, total, ...) that are
+left as None are read from the device tensors with .item(), which waits for the
+GPU: such a call is neither asynchronous nor capturable into a HIP graph. Pass
+them explicitly (and an output and workspace) to capture a call or to keep it
+asynchronous. With stream= given, outputs and workspaces the wrapper allocates
+are recorded on that stream, so torch does not reuse their memory before the
+call's kernels finish.
+
 Layout (see the header): K pool [pages][Hkv][16][128] (token-major), V pool
 [pages][Hkv][128][16] (dim-major), block table int32 [B][stride]. Pools are
 bf16, or uint8 OCP FP8 E4M3 codes with one scale per pool (value = code * scale).
@@ -62,6 +70,23 @@ def _stream(device: torch.device, stream) -> int:
     if stream is None:
         stream = torch.cuda.current_stream(device)
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _empty(shape, dtype: torch.dtype, device: torch.device, stream) -> torch.Tensor:
+    """torch.empty for an output or workspace of a call launched on `stream`.
+
+    torch's caching allocator ties a block to the stream that was current when it
+    was allocated. When the call runs on another stream (stream= given), the block
+    is also recorded on that stream, so that it is not handed to new work before
+    the call's kernels are done with it (a workspace the wrapper drops on return
+    would otherwise be reusable at once by work on the current stream)."""
+    t = torch.empty(shape, dtype=dtype, device=device)
+    if stream is not None:
+        s = stream if isinstance(stream, torch.cuda.Stream) else \
+            torch.cuda.ExternalStream(int(stream), device=device)
+        if s.cuda_stream != torch.cuda.current_stream(device).cuda_stream:
+            t.record_stream(s)
+    return t
 
 
 class PagedKV:
@@ -139,17 +164,17 @@ def decode(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor, max_kv_len: Opti
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out is None:
-        out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        out = _empty((B, Hq, D), torch.float32, dev, stream)
     _need(out, "out", torch.float32, dev)
     _shape(out, (B, Hq, HEAD_DIM), "out")
     if lse is None and want_lse:
-        lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        lse = _empty((B, Hq), torch.float32, dev, stream)
     if lse is not None:
         _need(lse, "lse", torch.float32, dev)
         _shape(lse, (B, Hq), "lse")
     ws_bytes = lib.rollout_attn_decode_workspace_size(B, Hq, kv.num_kv_heads, max_kv_len)
     if workspace is None:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        workspace = _empty(max(ws_bytes, 1), torch.uint8, dev, stream)
     _need(workspace, "workspace", torch.uint8, dev)
     s = kv.struct()
     _lib.check("rollout_attn_decode", lib.rollout_attn_decode(
@@ -193,18 +218,18 @@ def decode_shared_prefix(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor,
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out is None:
-        out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        out = _empty((B, Hq, D), torch.float32, dev, stream)
     _need(out, "out", torch.float32, dev)
     _shape(out, (B, Hq, HEAD_DIM), "out")
     if lse is None and want_lse:
-        lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        lse = _empty((B, Hq), torch.float32, dev, stream)
     if lse is not None:
         _need(lse, "lse", torch.float32, dev)
         _shape(lse, (B, Hq), "lse")
     ws_bytes = lib.rollout_attn_decode_shared_prefix_workspace_size(
         B, Hq, kv.num_kv_heads, max_kv_len, max_prefix_len)
     if workspace is None:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        workspace = _empty(max(ws_bytes, 1), torch.uint8, dev, stream)
     _need(workspace, "workspace", torch.uint8, dev)
     s = kv.struct()
     _lib.check("rollout_attn_decode_shared_prefix", lib.rollout_attn_decode_shared_prefix(
@@ -241,17 +266,17 @@ def append(q: torch.Tensor, cu_q: torch.Tensor, ctx_lens: torch.Tensor, kv: Page
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out is None:
-        out = torch.empty((total_q, Hq, D), dtype=torch.float32, device=dev)
+        out = _empty((total_q, Hq, D), torch.float32, dev, stream)
     _need(out, "out", torch.float32, dev)
     _shape(out, (total_q, Hq, HEAD_DIM), "out")
     if lse is None and want_lse:
-        lse = torch.empty((total_q, Hq), dtype=torch.float32, device=dev)
+        lse = _empty((total_q, Hq), torch.float32, dev, stream)
     if lse is not None:
         _need(lse, "lse", torch.float32, dev)
         _shape(lse, (total_q, Hq), "lse")
     ws_bytes = lib.rollout_attn_append_workspace_size(B, Hq, kv.num_kv_heads, max_q_len)
     if workspace is None:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        workspace = _empty(max(ws_bytes, 1), torch.uint8, dev, stream)
     _need(workspace, "workspace", torch.uint8, dev)
     s = kv.struct()
     _lib.check("rollout_attn_append", lib.rollout_attn_append(
@@ -294,17 +319,17 @@ def append_write(q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, cu_q
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out is None:
-        out = torch.empty((total_q, Hq, D), dtype=torch.float32, device=dev)
+        out = _empty((total_q, Hq, D), torch.float32, dev, stream)
     _need(out, "out", torch.float32, dev)
     _shape(out, (total_q, Hq, HEAD_DIM), "out")
     if lse is None and want_lse:
-        lse = torch.empty((total_q, Hq), dtype=torch.float32, device=dev)
+        lse = _empty((total_q, Hq), torch.float32, dev, stream)
     if lse is not None:
         _need(lse, "lse", torch.float32, dev)
         _shape(lse, (total_q, Hq), "lse")
     ws_bytes = lib.rollout_attn_append_workspace_size(B, Hq, kv.num_kv_heads, max_q_len)
     if workspace is None:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        workspace = _empty(max(ws_bytes, 1), torch.uint8, dev, stream)
     _need(workspace, "workspace", torch.uint8, dev)
     s = kv.struct()
     if cos_sin is None:
@@ -377,20 +402,20 @@ def mixed(q_decode: torch.Tensor, kv_decode: PagedKV, kv_lens: torch.Tensor,
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out_decode is None:
-        out_decode = torch.empty((Bd, Hq, D), dtype=torch.float32, device=dev)
+        out_decode = _empty((Bd, Hq, D), torch.float32, dev, stream)
     if out_append is None:
-        out_append = torch.empty((total_q, Hq, D), dtype=torch.float32, device=dev)
+        out_append = _empty((total_q, Hq, D), torch.float32, dev, stream)
     _need(out_decode, "out_decode", torch.float32, dev)
     _shape(out_decode, (Bd, Hq, HEAD_DIM), "out_decode")
     _need(out_append, "out_append", torch.float32, dev)
     _shape(out_append, (total_q, Hq, HEAD_DIM), "out_append")
-    lse_d = torch.empty((Bd, Hq), dtype=torch.float32, device=dev) if want_lse else None
-    lse_a = torch.empty((total_q, Hq), dtype=torch.float32, device=dev) if want_lse else None
+    lse_d = _empty((Bd, Hq), torch.float32, dev, stream) if want_lse else None
+    lse_a = _empty((total_q, Hq), torch.float32, dev, stream) if want_lse else None
     ws_bytes = lib.rollout_attn_mixed_workspace_size(
         Bd, Ba, Hq, kv_decode.num_kv_heads, kv_append.num_kv_heads, max_kv_len_decode,
         max_q_len)
     if workspace is None:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        workspace = _empty(max(ws_bytes, 1), torch.uint8, dev, stream)
     _need(workspace, "workspace", torch.uint8, dev)
     sd, sa = kv_decode.struct(), kv_append.struct()
     _lib.check("rollout_attn_mixed", lib.rollout_attn_mixed(
@@ -464,9 +489,9 @@ def kv_page_gather(kv: PagedKV, lens: torch.Tensor, cu_out: torch.Tensor,
         total = int(cu_out[-1].item()) if B else 0
     if max_len is None:
         max_len = int(lens.max().item()) if B else 0
-    k_out = torch.empty((total, kv.num_kv_heads, HEAD_DIM),
-                        dtype=torch.uint8 if kv.fp8 else torch.bfloat16, device=dev)
-    v_out = torch.empty_like(k_out)
+    k_out = _empty((total, kv.num_kv_heads, HEAD_DIM),
+                   torch.uint8 if kv.fp8 else torch.bfloat16, dev, stream)
+    v_out = _empty(tuple(k_out.shape), k_out.dtype, dev, stream)
     s = kv.struct()
     _lib.check("kv_page_gather", lib.kv_page_gather(
         ctypes.byref(s), lens.data_ptr(), cu_out.data_ptr(), B, total, max_len,
@@ -498,17 +523,17 @@ def _token_logprob(h, W, targets, scale, out, lse, want_lse, workspace, stream, 
                              f"for V={V}, D={D}, got {tuple(W.shape)}")
     _shape(targets, (N,), "targets")
     if out is None:
-        out = torch.empty((N,), dtype=torch.float32, device=dev)
+        out = _empty((N,), torch.float32, dev, stream)
     _need(out, "out", torch.float32, dev)
     _shape(out, (N,), "out")
     if lse is None and want_lse:
-        lse = torch.empty((N,), dtype=torch.float32, device=dev)
+        lse = _empty((N,), torch.float32, dev, stream)
     if lse is not None:
         _need(lse, "lse", torch.float32, dev)
         _shape(lse, (N,), "lse")
     if workspace is None:
-        workspace = torch.empty(max(lib.token_logprob_workspace_size(N, V), 1),
-                                dtype=torch.uint8, device=dev)
+        workspace = _empty(max(lib.token_logprob_workspace_size(N, V), 1), torch.uint8, dev,
+                           stream)
     _need(workspace, "workspace", torch.uint8, dev)
     fn = lib.token_logprob if packed_V is None else lib.token_logprob_packed
     name = "token_logprob" if packed_V is None else "token_logprob_packed"
@@ -539,7 +564,7 @@ def token_logprob_pack_weight(W: torch.Tensor, out: Optional[torch.Tensor] = Non
     V, D = W.shape
     n = lib.token_logprob_packed_weight_size(V, D) // 2
     if out is None:
-        out = torch.empty((max(n, 1),), dtype=torch.bfloat16, device=dev)
+        out = _empty((max(n, 1),), torch.bfloat16, dev, stream)
     _need(out, "out", torch.bfloat16, dev)
     _lib.check("token_logprob_pack_weight", lib.token_logprob_pack_weight(
         W.data_ptr(), V, D, out.data_ptr(), out.numel() * 2, _stream(dev, stream)))

@@ -31,6 +31,22 @@ void launch_split(bool fp8, dim3 grid, const DecodeArgs &a, hipStream_t stream) 
                        0, stream, a);
 }
 
+// Split length forced by the environment (RA_SPLIT_TOKENS, for testing the
+// split and combine paths), read once per process: a decimal number of keys
+// in [128, 65536], rounded up to a multiple of 128; anything else (absent,
+// not a number, out of range) leaves the planned length. 0 when unset.
+int64_t split_override() {
+  static const int64_t value = [] {
+    const char *env = getenv("RA_SPLIT_TOKENS");
+    if (!env || !*env) return (int64_t)0;
+    char *end = nullptr;
+    const long long v = strtoll(env, &end, 10);
+    if (*end != '\0' || v < 128 || v > 65536) return (int64_t)0;
+    return (int64_t)((v + 127) / 128 * 128);
+  }();
+  return value;
+}
+
 }  // namespace
 
 DecodePlan decode_plan(int32_t B, int32_t hkv, int32_t max_kv_len) {
@@ -43,10 +59,7 @@ DecodePlan decode_plan(int32_t B, int32_t hkv, int32_t max_kv_len) {
   int64_t work = (int64_t)B * hkv * (int64_t)(max_kv_len > 0 ? max_kv_len : 1);
   int64_t split = 512;
   while (split < 4096 && work / split > 8192) split *= 2;
-  if (const char *env = getenv("RA_SPLIT_TOKENS")) {
-    const long v = strtol(env, nullptr, 10);
-    if (v >= 128) split = (v + 127) / 128 * 128;
-  }
+  if (const int64_t forced = split_override()) split = forced;
   DecodePlan p;
   p.split_tokens = (int32_t)split;
   p.max_splits = (int32_t)((max_kv_len + split - 1) / split);

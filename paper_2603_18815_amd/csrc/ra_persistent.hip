@@ -26,6 +26,8 @@
 // A decode split is computed as by the decode split kernel but with 8 waves;
 // the decode combine follows as in plain decode. Results do not depend on
 // the order in which entries are taken.
+#include <atomic>
+
 #include "ra_append_tile.h"
 #include "ra_decode_split.h"
 #include "ra_internal.h"
@@ -272,6 +274,26 @@ __global__ __launch_bounds__(kMixThreads, 1) void mixed_kernel(MixedArgs m) {
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Compute units of the current device, queried once per device (a device's
+// count never changes; racing first calls store the same value).
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+hipError_t device_cus(int *cus) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices)
+    return hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
+  int n = g_cus[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if ((e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+      return e;
+    g_cus[dev].store(n, std::memory_order_relaxed);
+  }
+  *cus = n;
+  return hipSuccess;
+}
+
 }  // namespace
 
 MixedLayout mixed_layout(int32_t B_decode, int32_t B_append, int32_t hq, int32_t hkv_decode,
@@ -329,11 +351,8 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   if (e != hipSuccess) return e;
   // One workgroup per CU: the kernel's registers allow one 8-wave
   // workgroup per CU, and every workgroup runs until the entries run out.
-  int dev = 0, cus = 0;
-  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) !=
-      hipSuccess)
-    return e;
+  int cus = 0;
+  if ((e = device_cus(&cus)) != hipSuccess) return e;
   const int64_t entries = layout.max_tiles + layout.max_splits;
   const unsigned grid = (unsigned)(entries < cus ? (entries > 0 ? entries : 1) : cus);
   const dim3 g(grid), b(kMixThreads);

@@ -6,9 +6,11 @@ only draws lengths, lays trajectories out on shuffled physical pages, and fills
 pools and queries with bf16 N(0, 1) values.
 
 Workload shapes follow the multi-turn agent rollouts of the ProRL Agent paper:
-trajectories span dozens of turns and tens of thousands of tokens (Sec. 1), each
-agent step decodes over the whole history (Sec. 3.3.2), and tool or environment
-observations are appended to the retained token sequence (Sec. 3.3.3).
+a single agent trajectory can run for many tens of turns and grow to many
+thousands of tokens, into the tens of thousands (Sec. 1); every agent step
+decodes over the whole history kept so far (Sec. 3.3.2); and the output of a
+tool or of the environment is added after the tokens already kept
+(Sec. 3.3.3).
 
 Recipe (every choice the workload descriptions leave open is stated here):
   * lengths and page permutations: numpy.random.default_rng(seed);
