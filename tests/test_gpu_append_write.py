@@ -13,7 +13,7 @@ import torch
 import oracle
 import paper_2603_18815_amd as ra
 import synth
-from tests.gpu_util import assert_attn_close, bits
+from tests.gpu_util import APPEND_LSE_ATOL, assert_attn_close, bits
 
 pytestmark = pytest.mark.gpu
 SCALE = 1.0 / math.sqrt(128)
@@ -71,7 +71,7 @@ def test_append_write_equals_write_then_append(device, Hq, Hkv):
     ref, ref_lse = oracle.append(bits(q), cu, ctx, bits(s[2]), bits(s[3]), lay.block_table,
                                  SCALE)
     assert_attn_close(f[0].cpu().numpy(), ref, f"append_write G={Hq // Hkv}")
-    np.testing.assert_allclose(f[1].cpu().numpy(), ref_lse, atol=2e-3, rtol=0)
+    np.testing.assert_allclose(f[1].cpu().numpy(), ref_lse, atol=APPEND_LSE_ATOL, rtol=0)
 
 
 def test_append_write_full_append_workload(device):
@@ -124,4 +124,4 @@ def test_append_write_fp8_equals_write_then_append(device, Hq, Hkv):
     assert np.array_equal(bits(f[2]), kx) and np.array_equal(bits(f[3]), vx)
     ref, ref_lse = oracle.append_fp8(bits(q), cu, ctx, kx, vx, ks, vs, lay.block_table, SCALE)
     assert_attn_close(f[0].cpu().numpy(), ref, f"append_write fp8 G={Hq // Hkv}")
-    np.testing.assert_allclose(f[1].cpu().numpy(), ref_lse, atol=2e-3, rtol=0)
+    np.testing.assert_allclose(f[1].cpu().numpy(), ref_lse, atol=APPEND_LSE_ATOL, rtol=0)
