@@ -371,3 +371,41 @@ def test_rope_validation(lib):
     assert fused(rows=60) == _lib.RA_ERR_SHAPE          # max_kv_len 64 needs 64 rows
     assert fused(ws_bytes=16) == _lib.RA_ERR_WORKSPACE
     assert fused(total_q=0) == _lib.RA_OK
+
+
+def _decode_ws_sizes(env_value):
+    """Decode workspace sizes computed in a fresh process (the split override is
+    read once per process) with RA_SPLIT_TOKENS set to env_value (None: unset)."""
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r); from paper_2603_18815_amd import _lib; "
+            "f = _lib.load().rollout_attn_decode_workspace_size; "
+            "print(f(64, 32, 8, 32768), f(2, 8, 2, 1000), f(1, 1, 1, 65536))" % ROOT)
+    env = dict(os.environ)
+    env.pop("RA_SPLIT_TOKENS", None)
+    if env_value is not None:
+        env["RA_SPLIT_TOKENS"] = env_value
+    out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
+                         timeout=120, check=True).stdout.split()
+    return tuple(int(v) for v in out)
+
+
+def test_split_override_is_bounded():
+    """RA_SPLIT_TOKENS forces the decode split length only for values in
+    [128, 65536] (rounded up to a multiple of 128); anything else - too large for
+    an int32, negative, below 128, not a number - leaves the planned split, so
+    the workspace size (and the split arithmetic) stays that of no override."""
+    def expect(B, Hq, Hkv, L, split):
+        return B * Hq * max(1, -(-L // split)) * (128 + 2) * 4
+
+    planned = _decode_ws_sizes(None)
+    for bad in ("4294967296", "9223372036854775807", "-512", "127", "65537", "12x", "", "abc"):
+        assert _decode_ws_sizes(bad) == planned, bad
+    # in range: the split is the value rounded up to a multiple of 128
+    assert _decode_ws_sizes("128") == (expect(64, 32, 8, 32768, 128), expect(2, 8, 2, 1000, 128),
+                                       expect(1, 1, 1, 65536, 128))
+    assert _decode_ws_sizes("200") == (expect(64, 32, 8, 32768, 256), expect(2, 8, 2, 1000, 256),
+                                       expect(1, 1, 1, 65536, 256))
+    assert _decode_ws_sizes("65536") == (expect(64, 32, 8, 32768, 65536),
+                                         expect(2, 8, 2, 1000, 65536),
+                                         expect(1, 1, 1, 65536, 65536))

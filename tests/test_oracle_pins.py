@@ -596,6 +596,49 @@ def test_rope_is_the_complex_rotation_of_dim_pairs():
     assert np.mean(y == bits_f64(bf16_bits(ref))) > 0.99
 
 
+def test_rope_bits_follow_the_stated_fp32_rounding():
+    """The rotation's rounding, restated independently: numpy float32 products
+    x_i c_i, x_{i+64} s_i, x_{i+64} c_i, x_i s_i (each rounded to fp32), numpy
+    float32 difference and sum (rounded to fp32), then torch's round-to-nearest-
+    even conversion to bf16. The oracle must equal it on every element, bit for
+    bit. On the same inputs the two plausible other readings (the rotation in
+    fp64 rounded once to bf16; fused multiply-adds, x_i c_i - x_{i+64} s_i with
+    one rounding) differ from it on some elements, so the pin tells them apart."""
+    rng = np.random.default_rng(25)
+    N, H = 512, 4
+    x = randn_bits(rng, (N, H, 128))
+    # a few large and tiny magnitudes, and exact zeros, among the normal values
+    x[0, 0, :8] = bf16_bits(np.array([3e38, -3e38, 1e-38, -1e-38, 0.0, -0.0, 65504.0, 1e-5]))
+    table = _rope_table(1e6, np.arange(40000))
+    pos = rng.integers(0, 40000, N).astype(np.int32)
+    got = oracle.rope(x, pos, table)
+
+    xf = bits_f64(x).astype(np.float32)
+    lo, hi = xf[..., :64], xf[..., 64:]
+    c = table[pos, None, :64]
+    s = table[pos, None, 64:]
+    with np.errstate(over="ignore", invalid="ignore"):
+        y_lo = np.float32(lo * c) - np.float32(hi * s)
+        y_hi = np.float32(hi * c) + np.float32(lo * s)
+    y32 = np.concatenate([y_lo, y_hi], axis=-1)
+    assert y32.dtype == np.float32
+    want = torch.from_numpy(y32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, want)
+
+    # the alternative readings differ from this one somewhere
+    lo64, hi64 = lo.astype(np.float64), hi.astype(np.float64)
+    c64, s64 = c.astype(np.float64), s.astype(np.float64)
+    with np.errstate(over="ignore", invalid="ignore"):
+        f64 = np.concatenate([lo64 * c64 - hi64 * s64, hi64 * c64 + lo64 * s64], axis=-1)
+        fma = np.concatenate([(lo64 * c64 - np.float32(hi * s)).astype(np.float32),
+                              (hi64 * c64 + np.float32(lo * s)).astype(np.float32)], axis=-1)
+    once = torch.from_numpy(f64.astype(np.float32)).to(torch.bfloat16)
+    fused = torch.from_numpy(fma).to(torch.bfloat16)
+    for alt in (once, fused):
+        alt_bits = alt.view(torch.int16).numpy().view(np.uint16)
+        assert np.any(alt_bits != want)
+
+
 def test_rope_scores_depend_on_relative_position_only():
     """<rot(q, p1), rot(k, p2)> is a function of p1 - p2: shifting both
     positions by d changes it only by bf16 rounding."""
