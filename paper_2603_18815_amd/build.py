@@ -1,7 +1,8 @@
-"""Build librollout_attn.so (HIP, gfx950) in-tree with hipcc.
+"""Build librollout_attn.so (HIP, gfx950) in-tree with hipcc, and the
+hardware-ceiling microbenchmarks libra_microbench.so beside it.
 
 Every HIP source is compiled for gfx950 only, with packed-fp32 instruction
-selection disabled, then linked into one shared library next to this file.
+selection disabled, then linked into shared libraries next to this file.
 """
 import concurrent.futures
 import os
@@ -17,6 +18,8 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "librollout_attn.so")
 SOURCES = ["ra_api.hip", "ra_page.hip", "ra_decode.hip", "ra_persistent.hip",
            "ra_logprob.hip"]
+MICROBENCH_LIB = os.path.join(HERE, "libra_microbench.so")
+MICROBENCH_SOURCES = ["ra_microbench.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -43,16 +46,22 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib: str, verbose: bool) -> None:
+    tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    srcs = SOURCES + MICROBENCH_SOURCES
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = dict(zip(srcs, ex.map(lambda s: _compile(s, verbose), srcs)))
+    _link([objs[s] for s in SOURCES], LIB, verbose)
+    _link([objs[s] for s in MICROBENCH_SOURCES], MICROBENCH_LIB, verbose)
     return LIB
 
 

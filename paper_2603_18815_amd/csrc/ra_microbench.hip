@@ -1,0 +1,147 @@
+// Hardware ceilings measured on the GPU: matrix-core rate and shader clock,
+// LDS read bandwidth, streaming and paged HBM read rates. Declared in
+// include/ra_microbench.h.
+#include "ra_microbench.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kChains = 4;   // independent accumulators per wave
+
+__device__ __forceinline__ void clock_pair(int64_t *dst) {
+  dst[0] = (int64_t)__builtin_amdgcn_s_memtime();
+  dst[1] = (int64_t)__builtin_amdgcn_s_memrealtime();
+}
+
+__global__ __launch_bounds__(RA_MB_MFMA_THREADS) void mfma_kernel(const uint16_t *operands,
+                                                                  int iters, float *sink,
+                                                                  int64_t *clocks) {
+  const int tid = threadIdx.x;
+  bf16x8 a[kChains], b[kChains];
+#pragma unroll
+  for (int c = 0; c < kChains; ++c) {
+    a[c] = *reinterpret_cast<const bf16x8 *>(operands + (tid * 2 * kChains + c) * 8);
+    b[c] = *reinterpret_cast<const bf16x8 *>(operands + (tid * 2 * kChains + kChains + c) * 8);
+  }
+  f32x16 acc[kChains];
+#pragma unroll
+  for (int c = 0; c < kChains; ++c) acc[c] = f32x16{};
+  const bool timer = blockIdx.x == 0 && tid == 0;
+  int64_t t[4];
+  if (timer) clock_pair(t);
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int c = 0; c < kChains; ++c)
+      acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[c], b[c], acc[c], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += acc[c][r];
+  if (timer) {
+    clock_pair(t + 2);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) clocks[k] = t[k];
+  }
+  sink[(size_t)blockIdx.x * RA_MB_MFMA_THREADS + tid] = s;
+}
+
+constexpr int kLdsWords = 4096;   // 16-byte words of LDS read (64 KiB)
+
+__global__ __launch_bounds__(RA_MB_LDS_THREADS) void lds_kernel(int iters, uint32_t *sink,
+                                                                int64_t *clocks) {
+  __shared__ u32x4 buf[kLdsWords];
+  const int tid = threadIdx.x;
+  for (int k = tid; k < kLdsWords; k += RA_MB_LDS_THREADS)
+    buf[k] = u32x4{(uint32_t)k, (uint32_t)k * 3u, (uint32_t)k * 5u, (uint32_t)k * 7u};
+  __syncthreads();
+  u32x4 acc0 = {}, acc1 = {};
+  const bool timer = blockIdx.x == 0 && tid == 0;
+  int64_t t[4];
+  if (timer) clock_pair(t);
+  for (int i = 0; i < iters; ++i) {
+    // base <= 2047, so base + 256 k <= 3839 stays inside buf
+    const int base = (tid + 64 * (i & 15)) & 2047;
+    // three-input adds (v_add3_u32): two vector instructions per 16 bytes read
+#pragma unroll
+    for (int k = 0; k < 8; k += 4) {
+      acc0 = acc0 + buf[base + 256 * k] + buf[base + 256 * (k + 1)];
+      acc1 = acc1 + buf[base + 256 * (k + 2)] + buf[base + 256 * (k + 3)];
+    }
+  }
+  const u32x4 acc = acc0 + acc1;
+  if (timer) {
+    clock_pair(t + 2);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) clocks[k] = t[k];
+  }
+  sink[(size_t)blockIdx.x * RA_MB_LDS_THREADS + tid] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+}
+
+constexpr int kStreamThreads = 256;
+constexpr int kBlockWords = 4096 / 16;   // 16-byte words per 4 KiB block
+
+__global__ __launch_bounds__(kStreamThreads) void stream_kernel(const u32x4 *src, int64_t nblk,
+                                                                const int32_t *order,
+                                                                uint32_t *sink) {
+  const int tid = threadIdx.x;
+  u32x4 acc0 = {}, acc1 = {};
+  int64_t j = blockIdx.x;
+  const int64_t step = gridDim.x;
+  // two blocks per round, so that two 16-byte loads per lane are in flight
+  for (; j + step < nblk; j += 2 * step) {
+    int64_t b0 = j, b1 = j + step;
+    if (order) {
+      b0 = min(max((int64_t)order[b0], (int64_t)0), nblk - 1);
+      b1 = min(max((int64_t)order[b1], (int64_t)0), nblk - 1);
+    }
+    acc0 ^= __builtin_nontemporal_load(&src[b0 * kBlockWords + tid]);
+    acc1 ^= __builtin_nontemporal_load(&src[b1 * kBlockWords + tid]);
+  }
+  if (j < nblk) {
+    int64_t b0 = j;
+    if (order) b0 = min(max((int64_t)order[b0], (int64_t)0), nblk - 1);
+    acc0 ^= src[b0 * kBlockWords + tid];
+  }
+  const u32x4 acc = acc0 ^ acc1;
+  sink[(size_t)blockIdx.x * kStreamThreads + tid] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+}
+
+int launched() { return hipGetLastError() == hipSuccess ? 0 : 5; }
+
+}  // namespace
+
+extern "C" {
+
+int ra_mb_mfma_bf16(const void *operands, int32_t blocks, int32_t iters, float *sink,
+                    int64_t *clocks, hipStream_t stream) {
+  if (!operands || !sink || !clocks) return 1;
+  if (blocks <= 0 || iters <= 0) return 2;
+  hipLaunchKernelGGL(mfma_kernel, dim3(blocks), dim3(RA_MB_MFMA_THREADS), 0, stream,
+                     static_cast<const uint16_t *>(operands), iters, sink, clocks);
+  return launched();
+}
+
+int ra_mb_lds_read(int32_t blocks, int32_t iters, uint32_t *sink, int64_t *clocks,
+                   hipStream_t stream) {
+  if (!sink || !clocks) return 1;
+  if (blocks <= 0 || iters <= 0) return 2;
+  hipLaunchKernelGGL(lds_kernel, dim3(blocks), dim3(RA_MB_LDS_THREADS), 0, stream, iters, sink,
+                     clocks);
+  return launched();
+}
+
+int ra_mb_stream_read(const void *src, int64_t bytes, const int32_t *order, int32_t blocks,
+                      uint32_t *sink, hipStream_t stream) {
+  if (!src || !sink) return 1;
+  if (bytes <= 0 || bytes % 4096 != 0 || blocks <= 0) return 2;
+  hipLaunchKernelGGL(stream_kernel, dim3(blocks), dim3(kStreamThreads), 0, stream,
+                     static_cast<const u32x4 *>(src), bytes / 4096, order, sink);
+  return launched();
+}
+
+}  // extern "C"
