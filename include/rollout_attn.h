@@ -152,6 +152,26 @@ int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_
                         void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Decode that allocates nothing, for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc. Arguments, results and errors are
+ * those of rollout_attn_decode without the workspace; the split partial
+ * results go to a scratch array of RA_NOALLOC_SCRATCH_BYTES that the library
+ * holds in each GPU's memory until the process ends. A call whose
+ * rollout_attn_decode_workspace_size(B, Hq, Hkv, max_kv_len) exceeds
+ * RA_NOALLOC_SCRATCH_BYTES returns RA_ERR_WORKSPACE before any HIP call (64
+ * MiB holds, e.g., 64 rows of 32 query heads at up to 32768 keys). Every call
+ * on one GPU uses that GPU's one array and leaves its contents behind: calls
+ * that overlap in time on one GPU (different streams, or threads whose calls
+ * are in flight together) race and give wrong results; issue them on one
+ * stream.
+ */
+#define RA_NOALLOC_SCRATCH_BYTES (64u << 20)
+int rollout_attn_decode_noalloc(const void *q, const ra_paged_kv *kv, const int32_t *kv_lens,
+                                int32_t B, int32_t Hq, int32_t max_kv_len, float scale,
+                                float *out, float *lse, hipStream_t stream);
+
+/*
  * Shared-prefix decode: decode for groups of rows whose caches begin with the
  * same physical pages, e.g. the rollouts of one task, which share its prompt
  * (Sec. 4 generates several rollouts per task instance; Sec. 3.3.2 keeps all

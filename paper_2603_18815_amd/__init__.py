@@ -32,7 +32,7 @@ from ._lib import RolloutAttnError  # noqa: F401  (re-export)
 PAGE_SIZE = 16
 HEAD_DIM = 128
 
-__all__ = ["PagedKV", "decode", "decode_shared_prefix", "append", "append_write", "mixed",
+__all__ = ["PagedKV", "decode", "decode_noalloc", "decode_shared_prefix", "append", "append_write", "mixed",
            "kv_page_write",
            "kv_page_gather", "token_logprob", "decode_workspace_size",
            "decode_shared_prefix_workspace_size", "append_workspace_size", "mixed_workspace_size",
@@ -180,6 +180,37 @@ def decode(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor, max_kv_len: Opti
     _lib.check("rollout_attn_decode", lib.rollout_attn_decode(
         q.data_ptr(), ctypes.byref(s), kv_lens.data_ptr(), B, Hq, max_kv_len, float(scale),
         out.data_ptr(), _ptr(lse), workspace.data_ptr(), workspace.numel(), _stream(dev, stream)))
+    return out, lse
+
+
+def decode_noalloc(q: torch.Tensor, kv: PagedKV, kv_lens: torch.Tensor, max_kv_len: int,
+                   out: torch.Tensor, scale: Optional[float] = None,
+                   lse: Optional[torch.Tensor] = None, stream=None
+                   ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """decode() without a workspace: the library's own per-GPU device scratch holds
+    the split partials, so the call allocates nothing (the caller passes out, and
+    lse if wanted, and the host-side max_kv_len). Plans needing more than
+    RA_NOALLOC_SCRATCH_BYTES of partials are refused (RA_ERR_WORKSPACE). Calls
+    that overlap on one GPU share that scratch and race: keep them on one stream."""
+    lib = _lib.load()
+    dev = kv.device
+    _need(q, "q", torch.bfloat16, dev)
+    _need(kv_lens, "kv_lens", torch.int32, dev)
+    B, Hq, D = q.shape
+    _shape(q, (B, Hq, HEAD_DIM), "q")
+    _shape(kv_lens, (B,), "kv_lens")
+    _rows(kv, B)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    _need(out, "out", torch.float32, dev)
+    _shape(out, (B, Hq, HEAD_DIM), "out")
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+        _shape(lse, (B, Hq), "lse")
+    s = kv.struct()
+    _lib.check("rollout_attn_decode_noalloc", lib.rollout_attn_decode_noalloc(
+        q.data_ptr(), ctypes.byref(s), kv_lens.data_ptr(), B, Hq, int(max_kv_len), float(scale),
+        out.data_ptr(), _ptr(lse), _stream(dev, stream)))
     return out, lse
 
 

@@ -15,11 +15,14 @@ RA_ERR_HIP = 5
 RA_KV_BF16 = 0
 RA_KV_FP8_E4M3 = 1
 
+RA_NOALLOC_SCRATCH_BYTES = 64 << 20
+
 EXPORTS = (
     "ra_abi_version",
     "ra_status_string",
     "rollout_attn_decode_workspace_size",
     "rollout_attn_decode",
+    "rollout_attn_decode_noalloc",
     "rollout_attn_decode_shared_prefix_workspace_size",
     "rollout_attn_decode_shared_prefix",
     "rollout_attn_append_workspace_size",
@@ -84,6 +87,8 @@ def load() -> ctypes.CDLL:
     lib.rollout_attn_decode_workspace_size.restype = sz
     lib.rollout_attn_decode.argtypes = [vp, kvp, vp, i32, i32, i32, f32, vp, vp, vp, sz, vp]
     lib.rollout_attn_decode.restype = ctypes.c_int
+    lib.rollout_attn_decode_noalloc.argtypes = [vp, kvp, vp, i32, i32, i32, f32, vp, vp, vp]
+    lib.rollout_attn_decode_noalloc.restype = ctypes.c_int
     lib.rollout_attn_decode_shared_prefix_workspace_size.argtypes = [i32, i32, i32, i32, i32]
     lib.rollout_attn_decode_shared_prefix_workspace_size.restype = sz
     lib.rollout_attn_decode_shared_prefix.argtypes = [vp, kvp, vp, vp, vp, i32, i32, i32, i32,

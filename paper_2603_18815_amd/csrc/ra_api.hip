@@ -2,7 +2,9 @@
 // call), launch planning and status codes. See include/rollout_attn.h.
 #include "rollout_attn.h"
 
+#include <atomic>
 #include <cmath>
+#include <mutex>
 
 #include "ra_internal.h"
 
@@ -52,6 +54,50 @@ ra::PagedKV to_internal(const ra_paged_kv *kv) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? RA_OK : RA_ERR_HIP; }
 
+// Device scratch of rollout_attn_decode_noalloc: the decode split partials of
+// one call. Each GPU the library runs on holds its own copy for the life of
+// the process. In host code `scratch` names a host-side stand-in, not device
+// memory: only the per-device address from hipGetSymbolAddress is used.
+__device__ __align__(256) unsigned char scratch[RA_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+// Address of the current device's scratch, looked up once per device (with
+// that device current) and kept.
+hipError_t device_scratch(void **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void *p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+      if (!p) return hipErrorInvalidSymbol;
+      g_scratch[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return hipSuccess;
+}
+
+// Checks shared by rollout_attn_decode and rollout_attn_decode_noalloc.
+int check_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_lens, int32_t B,
+                 int32_t Hq, int32_t max_kv_len, float scale, const float *out) {
+  if (B < 0 || Hq <= 0 || max_kv_len < 0 || !std::isfinite(scale)) return RA_ERR_SHAPE;
+  int s = check_kv(kv);
+  if (s != RA_OK) return s;
+  if (!q || !kv_lens || !out) return RA_ERR_NULL;
+  if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
+  if (Hq / kv->num_kv_heads > 32 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
+  if (!positions_fit(kv, max_kv_len)) return RA_ERR_SHAPE;
+  return RA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -73,13 +119,8 @@ size_t rollout_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
 int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_lens, int32_t B,
                         int32_t Hq, int32_t max_kv_len, float scale, float *out, float *lse,
                         void *workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (B < 0 || Hq <= 0 || max_kv_len < 0 || !std::isfinite(scale)) return RA_ERR_SHAPE;
-  int s = check_kv(kv);
+  const int s = check_decode(q, kv, kv_lens, B, Hq, max_kv_len, scale, out);
   if (s != RA_OK) return s;
-  if (!q || !kv_lens || !out) return RA_ERR_NULL;
-  if (Hq % kv->num_kv_heads != 0) return RA_ERR_SHAPE;
-  if (Hq / kv->num_kv_heads > 32 || B > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
-  if (!positions_fit(kv, max_kv_len)) return RA_ERR_SHAPE;
   if (B == 0) return RA_OK;
   const ra::DecodePlan plan = ra::decode_plan(B, kv->num_kv_heads, max_kv_len);
   if (!workspace || workspace_bytes < ra::decode_workspace_bytes(B, Hq, plan))
@@ -87,6 +128,21 @@ int rollout_attn_decode(const void *q, const ra_paged_kv *kv, const int32_t *kv_
   return hip_status(ra::launch_decode(static_cast<const uint16_t *>(q), to_internal(kv), kv_lens,
                                       B, Hq, max_kv_len, scale, out, lse, workspace, plan,
                                       stream));
+}
+
+int rollout_attn_decode_noalloc(const void *q, const ra_paged_kv *kv, const int32_t *kv_lens,
+                                int32_t B, int32_t Hq, int32_t max_kv_len, float scale,
+                                float *out, float *lse, hipStream_t stream) {
+  const int s = check_decode(q, kv, kv_lens, B, Hq, max_kv_len, scale, out);
+  if (s != RA_OK) return s;
+  if (B == 0) return RA_OK;
+  const ra::DecodePlan plan = ra::decode_plan(B, kv->num_kv_heads, max_kv_len);
+  if (ra::decode_workspace_bytes(B, Hq, plan) > RA_NOALLOC_SCRATCH_BYTES) return RA_ERR_WORKSPACE;
+  void *ws = nullptr;
+  const hipError_t e = device_scratch(&ws);
+  if (e != hipSuccess) return RA_ERR_HIP;
+  return hip_status(ra::launch_decode(static_cast<const uint16_t *>(q), to_internal(kv), kv_lens,
+                                      B, Hq, max_kv_len, scale, out, lse, ws, plan, stream));
 }
 
 size_t rollout_attn_decode_shared_prefix_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,

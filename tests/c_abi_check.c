@@ -56,6 +56,22 @@ int main(void) {
   expect("decode: no rows",
          rollout_attn_decode(fake, &kv, ifake, 0, 4, 64, 0.1f, ffake, NULL, ws, sizeof ws, 0),
          RA_OK);
+  expect("decode_noalloc: NULL out",
+         rollout_attn_decode_noalloc(fake, &kv, ifake, 2, 4, 64, 0.1f, NULL, NULL, 0),
+         RA_ERR_NULL);
+  {
+    /* 256 rows x 64 heads of up to 65536 keys need more partials than the scratch holds */
+    ra_paged_kv big = kv;
+    big.num_kv_heads = 8;
+    big.bt_stride = 4096;
+    expect("decode_noalloc: plan beyond the scratch",
+           rollout_attn_decode_noalloc(fake, &big, ifake, 256, 64, 65536, 0.1f, ffake, NULL, 0),
+           RA_ERR_WORKSPACE);
+    if (rollout_attn_decode_workspace_size(256, 64, 8, 65536) <= RA_NOALLOC_SCRATCH_BYTES) {
+      printf("FAIL decode_noalloc: the rejected plan fits the scratch\n");
+      ++failures;
+    }
+  }
   expect("shared-prefix decode: NULL group_start",
          rollout_attn_decode_shared_prefix(fake, &kv, ifake, NULL, ifake, 16, 4, 2, 8, 32, 64,
                                            0.1f, ffake, NULL, ws, sizeof ws, 0),

@@ -409,3 +409,22 @@ def test_split_override_is_bounded():
     assert _decode_ws_sizes("65536") == (expect(64, 32, 8, 32768, 65536),
                                          expect(2, 8, 2, 1000, 65536),
                                          expect(1, 1, 1, 65536, 65536))
+
+
+def test_decode_noalloc_validation(lib):
+    """The no-allocation decode checks arguments like decode and refuses, before
+    any HIP call, plans whose split partials exceed its scratch."""
+    f = lib.rollout_attn_decode_noalloc
+    kv = _kv()
+    assert f(None, ctypes.byref(kv), FAKE, 2, 4, 64, 0.1, FAKE, None, None) == _lib.RA_ERR_NULL
+    assert f(FAKE, ctypes.byref(kv), FAKE, 2, 4, 64, 0.1, None, None, None) == _lib.RA_ERR_NULL
+    assert f(FAKE, ctypes.byref(kv), FAKE, 2, 5, 64, 0.1, FAKE, None, None) == _lib.RA_ERR_SHAPE
+    assert f(FAKE, ctypes.byref(kv), FAKE, 0, 4, 64, 0.1, FAKE, None, None) == _lib.RA_OK
+    big = _kv(num_kv_heads=8, bt_stride=4096)
+    need = lib.rollout_attn_decode_workspace_size(256, 64, 8, 65536)
+    assert need > _lib.RA_NOALLOC_SCRATCH_BYTES
+    assert f(FAKE, ctypes.byref(big), FAKE, 256, 64, 65536, 0.1, FAKE, None,
+             None) == _lib.RA_ERR_WORKSPACE
+    # the Qwen3-8B decode workload (64 rows, 32 heads, up to 32768 keys) fits
+    assert lib.rollout_attn_decode_workspace_size(64, 32, 8, 32768) <= \
+        _lib.RA_NOALLOC_SCRATCH_BYTES
