@@ -35,7 +35,13 @@ and as one fused call.
 rollouts whose rows share each task's prompt pages. `token_logprob` times the
 fused LM-head log-probability kernel at the Qwen3-8B head for 64 and 1024
 tokens, with the head row-major and packed.
-`cpu_baseline` is the fp64 CPU oracle on a bounded sample of the same inputs.
+`long_horizon_decode` times decode of B = 256 trajectories with Hq = 64 and
+contexts log-normal around 16384 keys (up to 65536). `achievable` gives what this
+GPU delivers to the kernels, measured in the same run (matrix-core rate and
+clock, LDS reads, streaming and paged HBM reads).
+`cpu_baseline` is the fp64 CPU oracle on a bounded sample of the same inputs
+(`cpu_baseline_single_thread`: the small decode workload on one thread;
+`cpu_baseline_long_decode`: whole rows of the long-horizon workload).
 """
 import argparse
 import json
@@ -78,9 +84,11 @@ KERNEL_SOURCES = {
                "paper_2603_18815_amd/csrc/ra_append_tile.h",
                "paper_2603_18815_amd/csrc/ra_device.h"),
 }
+KERNEL_SOURCES["long_decode"] = KERNEL_SOURCES["decode"]
 TRAFFIC_FILES = {
     "decode": "profiles/decode_qwen3_8b_b64.hbm_traffic.txt",
     "append": "profiles/append_qwen3_8b_b32.hbm_traffic.txt",
+    "long_decode": "profiles/decode_long_horizon_b256.hbm_traffic.txt",
 }
 
 
@@ -170,7 +178,116 @@ def cpu_baseline(wd, td, wa, ta, seconds: float):
            "cpu_model": cpu_model,
            "sample": f"append, {nq} single queries (all heads) drawn from random rows of the "
                      f"append workload, {spent_a:.1f} s wall"}
-    return dec, app
+    # the small decode workload (B = 4, Hq = 8, Hkv = 2) in full, on one thread
+    import synth
+    w1 = synth.config(1)
+    t1 = synth.make_tensors(w1, dev)
+    k1, v1, bt1 = compact_rows(t1.k_pool, t1.v_pool, w1.decode_table(), w1.kv_lens)
+    q1 = bits(t1.q_decode)
+    del t1
+    oracle.set_num_threads(1)
+    try:
+        spent1, reps = 0.0, 0
+        while spent1 < min(seconds, 2.0):
+            t0 = time.perf_counter()
+            oracle.decode(q1, k1, v1, bt1, w1.kv_lens, SCALE)
+            spent1 += time.perf_counter() - t0
+            reps += 1
+    finally:
+        oracle.set_num_threads(cores)
+    single = {"value": decode_bytes(w1) * reps / spent1 / 1e9, "unit": "GB/s", "cores": 1,
+              "kind": "oracle", "cpu_model": cpu_model,
+              "sample": f"decode, the whole B=4 workload ({w1.name}) {reps} times on one thread, "
+                        f"{spent1:.2f} s wall"}
+    # the long-horizon decode workload (B = 256, Hq = 64): whole rows in a seeded order
+    w4 = synth.config(4)
+    t4 = synth.make_tensors(w4, dev)
+    order4 = np.random.default_rng(4).permutation(w4.kv_lens.shape[0])
+    table4 = w4.decode_table()
+    spent4, bytes4, rows4 = 0.0, 0, 0
+    for chunk in np.array_split(order4, 32):
+        k4, v4, bt4 = compact_rows(t4.k_pool, t4.v_pool, table4[chunk], w4.kv_lens[chunk])
+        q4 = bits(t4.q_decode[torch.as_tensor(chunk, device=dev)])
+        t0 = time.perf_counter()
+        oracle.decode(q4, k4, v4, bt4, w4.kv_lens[chunk], SCALE)
+        spent4 += time.perf_counter() - t0
+        sub = w4.kv_lens[chunk].astype(np.int64)
+        bytes4 += int((sub * w4.Hkv * 128 * 4 + w4.Hq * 128 * 6 + 4 * ((sub + 15) // 16)
+                       + 4).sum())
+        rows4 += len(chunk)
+        del k4, v4, q4
+        if spent4 > seconds:
+            break
+    del t4
+    torch.cuda.empty_cache()
+    long4 = {"value": bytes4 / spent4 / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
+             "cpu_model": cpu_model,
+             "sample": f"decode, {rows4} whole rows (all 64 heads) of the {w4.kv_lens.shape[0]}-row "
+                       f"long-horizon workload in a seeded order, {spent4:.1f} s wall"}
+    return dec, app, single, long4
+
+
+def long_decode_leg(ra, synth, dev, steps: int, warmup: int):
+    """Decode of the long-horizon workload: B = 256 trajectories, Hq = 64, Hkv = 8,
+    contexts log-normal around 16384 keys clipped to [512, 65536], shuffled pages
+    (split + combine kernels, one call per step)."""
+    import torch
+
+    w = synth.config(4)
+    t = synth.make_tensors(w, dev)
+    kv = ra.PagedKV(t.k_pool, t.v_pool, torch.as_tensor(w.decode_table(), device=dev))
+    lens = torch.as_tensor(w.kv_lens.astype(np.int32), device=dev)
+    B, max_kv = w.kv_lens.shape[0], int(w.kv_lens.max())
+    out = torch.empty((B, w.Hq, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty(ra.decode_workspace_size(B, w.Hq, w.Hkv, max_kv), dtype=torch.uint8,
+                     device=dev)
+    for _ in range(warmup):
+        ra.decode(t.q_decode, kv, lens, max_kv, SCALE, out=out, workspace=ws)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+    for e in ev:
+        e[0].record()
+        ra.decode(t.q_decode, kv, lens, max_kv, SCALE, out=out, workspace=ws)
+        e[1].record()
+    torch.cuda.synchronize()
+    ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    nbytes = decode_bytes(w)
+    gbs = nbytes / (ms.mean() * 1e-3) / 1e9
+    res = {"workload": w.name, "steps": steps, "warmup": warmup,
+           "rows": B, "kv_tokens": int(w.kv_lens.sum()),
+           "ms": round(float(ms.mean()), 4), "ms_median": round(float(np.median(ms)), 4),
+           "ms_min": round(float(ms.min()), 4), "algorithmic_bytes": nbytes,
+           "GB_s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+           "traffic": measured_traffic("long_decode")}
+    del t, kv, out, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def achievable_leg(dev):
+    """What this GPU delivers to the kernels, measured now by libra_microbench.so:
+    the bf16 matrix-core rate of the append kernel's product on random and on zero
+    operands with the shader clock it ran at, LDS read bandwidth, and HBM read
+    rates (streaming, and shuffled 4 KiB pages as a paged cache is read). Context
+    for the roofline fractions, which use the published peaks."""
+    import torch
+
+    from paper_2603_18815_amd import microbench as mb
+
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    res = {"compute_units": cus}
+    for name, zeros in (("mfma_bf16_random", False), ("mfma_bf16_zeros", True)):
+        tf, ghz = mb.mfma_bf16(2 * cus, 20000, zeros=zeros)
+        res[name] = {"TFLOP_s": round(tf, 1), "clock_GHz": round(ghz, 3),
+                     "peak_at_clock_TFLOP_s": round(cus * 4096 * ghz / 1e3, 1),
+                     "frac_of_published_peak": round(tf / BF16_PEAK_TFLOPS, 4)}
+    bpc, ghz, gbs = mb.lds_read(2 * cus, 20000)
+    res["lds_read"] = {"GB_s": round(gbs, 0), "clock_GHz": round(ghz, 3),
+                       "bytes_per_clock_per_CU": round(gbs / (cus * ghz), 1)}
+    for name, paged in (("hbm_read_stream", False), ("hbm_read_paged_4KiB", True)):
+        g = mb.stream_read(4 << 30, paged, 8 * cus)
+        res[name] = {"GB_s": round(g, 1), "frac_of_published_peak": round(g / HBM_PEAK_GBS, 4)}
+    torch.cuda.empty_cache()
+    return res
 
 
 def mixed_step(ra, synth, dev, steps: int, warmup: int):
@@ -556,13 +673,20 @@ def main():
                     help="skip the token log-probability leg (Qwen3-8B LM head)")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed-step leg (B = 512, 85 %% decode / 15 %% append rows)")
+    ap.add_argument("--no-long-decode", action="store_true",
+                    help="skip the long-horizon decode leg (B = 256, Hq = 64)")
+    ap.add_argument("--no-achievable", action="store_true",
+                    help="skip the hardware-ceiling microbenchmarks")
     ap.add_argument("--only", choices=["write", "decode", "append", "copy", "mixed", "logprob",
-                                       "decode_fp8", "append_fp8"],
+                                       "decode_fp8", "append_fp8", "long_decode", "mfma",
+                                       "stream"],
                     help="run only this part of the step --steps times after --warmup "
                          "(for rocprofv3 runs; 'copy' is a 1 GiB torch copy used to "
                          "calibrate the HBM byte counters, 'mixed' the mixed-step leg, "
                          "'logprob' the LM-head log-probability leg, 'decode_fp8' / 'append_fp8' "
-                         "the decode / append workload over fp8 pools); prints no JSON line")
+                         "the decode / append workload over fp8 pools, 'long_decode' the "
+                         "long-horizon decode, 'mfma' / 'stream' the matrix-core and HBM-read "
+                         "microbenchmarks); prints no JSON line")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path "
@@ -584,6 +708,20 @@ def main():
     if args.only == "logprob":
         res = logprob_leg(ra, synth, dev, args.steps, args.warmup)
         print(f"[bench] token_logprob {json.dumps(res)}", flush=True)
+        return
+    if args.only == "long_decode":
+        res = long_decode_leg(ra, synth, dev, args.steps, args.warmup)
+        print(f"[bench] long decode {json.dumps(res)}", flush=True)
+        return
+    if args.only in ("mfma", "stream"):
+        from paper_2603_18815_amd import microbench as mb
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        for _ in range(args.warmup + args.steps):
+            if args.only == "mfma":
+                tf, ghz = mb.mfma_bf16(2 * cus, 20000, reps=1)
+            else:
+                g = mb.stream_read(4 << 30, True, 8 * cus, reps=1)
+        print(f"[bench] ran {args.only} {args.warmup} + {args.steps} times", flush=True)
         return
     wd, wa = synth.config(2), synth.config(3)
     td, ta = synth.make_tensors(wd, dev), synth.make_tensors(wa, dev)
@@ -704,10 +842,16 @@ def main():
     mixed = None
     if not args.no_mixed:
         mixed = mixed_step(ra, synth, dev, min(args.steps, 10), min(args.warmup, 2))
+    long_decode = None
+    if not args.no_long_decode:
+        long_decode = long_decode_leg(ra, synth, dev, args.steps, args.warmup)
+    achievable = None
+    if not args.no_achievable:
+        achievable = achievable_leg(dev)
 
-    cpu_dec = cpu_app = None
+    cpu_dec = cpu_app = cpu_single = cpu_long = None
     if not args.no_cpu_baseline:
-        cpu_dec, cpu_app = cpu_baseline(wd, td, wa, ta, args.cpu_seconds)
+        cpu_dec, cpu_app, cpu_single, cpu_long = cpu_baseline(wd, td, wa, ta, args.cpu_seconds)
 
     rec = {
         "metric": "decode attn HBM GB/s (% of peak) + append TFLOP/s, Qwen3-8B GQA shape",
@@ -759,6 +903,8 @@ def main():
         "append_write": append_write,
         "fp8_kv_decode": fp8,
         "token_logprob": logprob,
+        "long_horizon_decode": long_decode,
+        "achievable": achievable,
         "paper_context": {
             "note": "the paper's own system-level rollout throughput, on its hardware; context "
                     "only, not comparable to the kernel metric (the paper publishes no kernel "
@@ -768,6 +914,8 @@ def main():
             "workload": "DAPO RL on SWE tasks"},
         "cpu_baseline": cpu_dec,
         "cpu_baseline_append": cpu_app,
+        "cpu_baseline_single_thread": cpu_single,
+        "cpu_baseline_long_decode": cpu_long,
     }
     print(json.dumps(rec), flush=True)
 

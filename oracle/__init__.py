@@ -39,6 +39,8 @@ def _load():
     lib.oracle_decode_f64.argtypes = [_u16p, _u16p, _u16p, _i32p, c_i64, _i32p, c_int, c_int,
                                       c_int, c_int, c_int, c_dbl, _f64p, _f64p]
     lib.oracle_decode_f64.restype = c_int
+    lib.oracle_set_num_threads.argtypes = [c_int]
+    lib.oracle_set_num_threads.restype = None
     lib.oracle_append_f64.argtypes = [_u16p, _i32p, _i32p, _u16p, _u16p, _i32p, c_i64, c_int,
                                       c_int, c_int, c_int, c_int, c_dbl, _f64p, _f64p]
     lib.oracle_append_f64.restype = c_int
@@ -83,6 +85,11 @@ def _load():
 def num_threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Set the OpenMP threads of the oracle's parallel loops (timing only)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def _u16(a):

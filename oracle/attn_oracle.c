@@ -440,3 +440,9 @@ int oracle_rope_bf16(const uint16_t *x, int64_t n_rows, int heads, const int32_t
 }
 
 int oracle_num_threads(void) { return omp_get_max_threads(); }
+
+/* Threads of the parallel loops that follow (timing only; results do not
+ * depend on it: each output element is computed by one thread). */
+void oracle_set_num_threads(int n) {
+  if (n > 0) omp_set_num_threads(n);
+}
