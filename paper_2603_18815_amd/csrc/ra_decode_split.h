@@ -188,7 +188,7 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
     bf16x8 ka[2][4];
     bf16x8 va[8];
     if constexpr (kFp8) {
-      // one byte per element: K rows as 2 x 16 bytes per lane, V as 8 bytes
+      // one byte per element: K rows as 2 x 16 bytes per lane
       const uint8_t *kb = reinterpret_cast<const uint8_t *>(a.k_pool) +
                           ((size_t)(ka_sel ? id1 : id0) * a.hkv + g) * head_stride;
 #pragma unroll
@@ -202,10 +202,19 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
         }
       const uint8_t *vb = reinterpret_cast<const uint8_t *>(a.v_pool) +
                           ((size_t)(sv_sel ? id1 : id0) * a.hkv + g) * head_stride;
+      // Whole 16-slot V rows, 16 bytes per lane: lane l loads row
+      // d = 16 (2 j + h) + col of its page (h = l / 16 % 2), so lanes l and
+      // l ^ 16 hold rows 2j and 2j + 1 of one page; one v_permlane16_swap per
+      // dword then leaves each lane the slots it supplies (8 h + 0..7) of both.
+      const int vh = (lane >> 4) & 1;
 #pragma unroll
-      for (int mt = 0; mt < 8; ++mt)
-        va[mt] = fp8x8_to_bf16x8(
-            *reinterpret_cast<const u32x2 *>(vb + (16 * mt + col) * kPage + sv_slot));
+      for (int j = 0; j < 4; ++j) {
+        const u32x4 w = *reinterpret_cast<const u32x4 *>(vb + (16 * (2 * j + vh) + col) * kPage);
+        const auto s0 = __builtin_amdgcn_permlane16_swap(w[0], w[2], false, false);
+        const auto s1 = __builtin_amdgcn_permlane16_swap(w[1], w[3], false, false);
+        va[2 * j] = fp8x8_to_bf16x8(u32x2{s0[0], s1[0]});
+        va[2 * j + 1] = fp8x8_to_bf16x8(u32x2{s0[1], s1[1]});
+      }
     } else {
       const uint16_t *kb =
           a.k_pool + ((size_t)(ka_sel ? id1 : id0) * a.hkv + g) * head_stride;
