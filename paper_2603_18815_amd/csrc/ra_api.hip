@@ -172,10 +172,14 @@ int rollout_attn_decode_shared_prefix(const void *q, const ra_paged_kv *kv,
   if (B == 0) return RA_OK;
   if (num_groups == 0 || max_group_rows == 0 || max_group_rows > B || num_groups > B)
     return RA_ERR_SHAPE;
-  const ra::SharedPrefixShape sh =
-      ra::shared_prefix_shape(Hq / kv->num_kv_heads, num_groups, max_group_rows);
-  if (sh.prefix_z > kMaxGridYZ || sh.row_z > kMaxGridYZ) return RA_ERR_UNSUPPORTED;
   const ra::DecodePlan plan = ra::decode_plan(B, kv->num_kv_heads, max_kv_len);
+  const ra::SharedPrefixShape sh = ra::shared_prefix_shape(Hq / kv->num_kv_heads, num_groups,
+                                                           max_group_rows, plan, max_prefix_len);
+  // grid z holds the prefix planes and the row planes; prefix item indices
+  // (plane x max_splits + split) must fit an int
+  if (sh.prefix_planes + sh.row_z > kMaxGridYZ ||
+      sh.prefix_planes * plan.max_splits > INT32_MAX)
+    return RA_ERR_UNSUPPORTED;
   if (!workspace ||
       workspace_bytes < ra::shared_prefix_workspace_bytes(B, Hq, plan, max_prefix_len))
     return RA_ERR_WORKSPACE;

@@ -21,6 +21,43 @@ __global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_kernel(De
   decode_split<NT, kPrefix, kSplitWaves, kFp8>(a, blockIdx.x, blockIdx.y, blockIdx.z, lds);
 }
 
+// Shared-prefix decode in one launch. Planes z < prefix_planes hold the
+// prefix items, item i = z * gridDim.y + y, with the chunks of one (group,
+// prefix split) adjacent so that the workgroups reading the same prefix pages
+// run close together (the later ones mostly hit the cache); the planes after
+// hold the row items as in plain decode. One launch lets the few prefix items
+// run beside the many row items instead of before them, in a pass of their own
+// that leaves most of the machine idle.
+template <int NT, bool kFp8>
+__global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_shared_kernel(
+    DecodeArgs a, int32_t prefix_planes, int32_t chunks, int32_t prefix_items) {
+  __shared__ DecodeLds<NT, kSplitWaves> lds;
+  const int z = blockIdx.z;
+  if (z < prefix_planes) {
+    const int i = z * gridDim.y + blockIdx.y;
+    if (i >= prefix_items) return;
+    const int sub = i % chunks, gs = i / chunks;
+    const int split = gs % a.prefix_slots, grp = gs / a.prefix_slots;
+    DecodeArgs p = a;
+    p.zdiv = chunks;
+    decode_split<NT, true, kSplitWaves, kFp8>(p, blockIdx.x, split, grp * chunks + sub, lds);
+  } else {
+    decode_split<NT, false, kSplitWaves, kFp8>(a, blockIdx.x, blockIdx.y, z - prefix_planes, lds);
+  }
+}
+
+template <int NT>
+void launch_shared(bool fp8, dim3 grid, const DecodeArgs &a, const SharedPrefixShape &sh,
+                   hipStream_t stream) {
+  const int32_t planes = (int32_t)sh.prefix_planes, items = (int32_t)sh.prefix_items;
+  if (fp8)
+    hipLaunchKernelGGL((decode_shared_kernel<NT, true>), grid, dim3(kSplitWaves * kWave), 0,
+                       stream, a, planes, sh.chunks, items);
+  else
+    hipLaunchKernelGGL((decode_shared_kernel<NT, false>), grid, dim3(kSplitWaves * kWave), 0,
+                       stream, a, planes, sh.chunks, items);
+}
+
 template <int NT, bool kPrefix>
 void launch_split(bool fp8, dim3 grid, const DecodeArgs &a, hipStream_t stream) {
   if (fp8)
@@ -99,12 +136,17 @@ hipError_t launch_decode(const uint16_t *q, const PagedKV &kv, const int32_t *kv
   return hipGetLastError();
 }
 
-SharedPrefixShape shared_prefix_shape(int32_t group, int32_t num_groups, int32_t max_group_rows) {
+SharedPrefixShape shared_prefix_shape(int32_t group, int32_t num_groups, int32_t max_group_rows,
+                                      const DecodePlan &plan, int32_t max_prefix_len) {
   SharedPrefixShape sh;
-  sh.rows_per_chunk = min(max_group_rows, 2 * 16 / group);
-  sh.tiles = (sh.rows_per_chunk * group + 15) / 16;
+  // as many rows per prefix chunk as fill the row items' tiles (one tile,
+  // two for groups of 17 to 32 heads), so that both kinds of item share one
+  // register and LDS budget
+  sh.tiles = group > 16 ? 2 : 1;
+  sh.rows_per_chunk = max(1, min(max_group_rows, 16 * sh.tiles / group));
   sh.chunks = (max_group_rows + sh.rows_per_chunk - 1) / sh.rows_per_chunk;
-  sh.prefix_z = (int64_t)num_groups * sh.chunks;
+  sh.prefix_items = (int64_t)num_groups * sh.chunks * prefix_slots(plan, max_prefix_len);
+  sh.prefix_planes = (sh.prefix_items + plan.max_splits - 1) / plan.max_splits;
   sh.row_z = (int64_t)num_groups * max_group_rows;
   return sh;
 }
@@ -119,28 +161,20 @@ hipError_t launch_decode_shared_prefix(const uint16_t *q, const PagedKV &kv,
   const int32_t ps = prefix_slots(plan, max_prefix_len);
   DecodeArgs a = make_decode_args(q, kv, kv_lens, B, hq, max_kv_len, scale, workspace,
                            plan.max_splits + ps, plan);
-  const SharedPrefixShape sh = shared_prefix_shape(a.group, num_groups, max_group_rows);
+  const SharedPrefixShape sh =
+      shared_prefix_shape(a.group, num_groups, max_group_rows, plan, max_prefix_len);
   a.group_start = group_start;
   a.prefix_len = prefix_len;
   a.prefix_slots = ps;
   a.rows_per_chunk = sh.rows_per_chunk;
-  hipError_t e = hipSuccess;
-  if (ps > 0) {
-    a.zdiv = sh.chunks;
-    const dim3 grid(kv.hkv, ps, (unsigned)sh.prefix_z);
-    if (sh.tiles == 1)
-      launch_split<1, true>(kv.fp8, grid, a, stream);
-    else
-      launch_split<2, true>(kv.fp8, grid, a, stream);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
   a.zdiv = max_group_rows;
-  const dim3 rows_grid(kv.hkv, plan.max_splits, (unsigned)sh.row_z);
-  if (a.group > 16)
-    launch_split<2, false>(kv.fp8, rows_grid, a, stream);
+  const dim3 grid(kv.hkv, plan.max_splits, (unsigned)(sh.prefix_planes + sh.row_z));
+  if (sh.tiles == 2)
+    launch_shared<2>(kv.fp8, grid, a, sh, stream);
   else
-    launch_split<1, false>(kv.fp8, rows_grid, a, stream);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+    launch_shared<1>(kv.fp8, grid, a, sh, stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(hq, (unsigned)sh.row_z), dim3(kHeadDim), 0, stream,
                      a, out, lse);
   return hipGetLastError();

@@ -8,7 +8,7 @@
 //   S^T[key][col] = K[key][:] · Q^T[:][col]       (4 x mfma 16x16x32 per 16 keys)
 //   O^T[d][col]  += V^T[d][key] · P^T[key][col]   (8 x mfma per 32 keys and tile)
 // The matrix columns are query rows that read the same keys: the G = Hq / Hkv
-// query heads of one row (plain decode), or the heads of up to 32 / G rows
+// query heads of one row (plain decode), or the heads of up to 16 NT / G rows
 // that share a prefix (shared-prefix decode), in NT tiles of 16 columns (zero
 // padded), so every KV byte is read once for all of them. Softmax is the
 // online (running max / running sum) form in fp32, in base 2 with log2(e)
@@ -26,6 +26,8 @@
 // Combine kernel: one workgroup per (row, query head) merges the slots in a
 // fixed order (prefix, then suffix):
 //   M = max_s m_s,  l = sum_s l_s 2^(m_s - M),  out = sum_s o_s 2^(m_s - M) / l.
+// It reads the slots eight at a time, so that a row's loads are in flight
+// together rather than one dependent round trip per slot.
 #pragma once
 
 #include "ra_device.h"
@@ -363,14 +365,32 @@ __global__ __launch_bounds__(kHeadDim) void decode_combine_kernel(DecodeArgs a, 
   const float *o = a.ws_o + bh * a.slots * kHeadDim + d;
   // slots in merge order: prefix splits [0, np), then suffix splits
   auto slot = [&](int s) { return s < np ? s : a.prefix_slots + (s - np); };
-  float M = m[slot(0)];
-  for (int s = 1; s < np + ns; ++s) M = fmaxf(M, m[slot(s)]);
+  const int n = np + ns;
+  constexpr int kBatch = 8;
+  float M = -INFINITY;
+  for (int s0 = 0; s0 < n; s0 += kBatch) {
+    float mv[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) mv[j] = s0 + j < n ? m[slot(s0 + j)] : -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) M = fmaxf(M, mv[j]);
+  }
   float acc = 0.f, lsum = 0.f;
-  for (int s = 0; s < np + ns; ++s) {
-    const int k = slot(s);
-    const float f = fast_exp2(m[k] - M);
-    acc += f * o[(size_t)k * kHeadDim];
-    lsum += f * l[k];
+  for (int s0 = 0; s0 < n; s0 += kBatch) {
+    float f[kBatch], ov[kBatch], lv[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const bool ok = s0 + j < n;
+      const int k = slot(ok ? s0 + j : s0);
+      ov[j] = o[(size_t)k * kHeadDim];
+      lv[j] = l[k];
+      f[j] = ok ? fast_exp2(m[k] - M) : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      acc += f[j] * ov[j];
+      lsum += f[j] * lv[j];
+    }
   }
   out[bh * kHeadDim + d] = acc / lsum * a.v_scale;
   if (lse && d == 0) lse[bh] = (M + __log2f(lsum)) * kLn2;

@@ -35,14 +35,17 @@ hipError_t launch_decode(const uint16_t *q, const PagedKV &kv, const int32_t *kv
                          void *workspace, const DecodePlan &plan, hipStream_t stream);
 
 // ---- shared-prefix decode (rows of a group share their first prefix pages) ----
-// Grid sizes of one call: a prefix workgroup covers rows_per_chunk rows of a
-// group (tiles 16-column tiles); prefix_z / row_z are the grid z extents.
+int32_t prefix_slots(const DecodePlan &plan, int32_t max_prefix_len);
+// Work of one call, all in one launch of grid (Hkv, max_splits, prefix_planes
+// + row_z): prefix_items (group chunk of rows_per_chunk rows, prefix split)
+// pairs folded over the first prefix_planes planes, then one plane per (group,
+// row slot). Both kinds of item use `tiles` 16-column tiles.
 struct SharedPrefixShape {
   int32_t rows_per_chunk, tiles, chunks;
-  int64_t prefix_z, row_z;
+  int64_t prefix_items, prefix_planes, row_z;
 };
-SharedPrefixShape shared_prefix_shape(int32_t group, int32_t num_groups, int32_t max_group_rows);
-int32_t prefix_slots(const DecodePlan &plan, int32_t max_prefix_len);
+SharedPrefixShape shared_prefix_shape(int32_t group, int32_t num_groups, int32_t max_group_rows,
+                                      const DecodePlan &plan, int32_t max_prefix_len);
 size_t shared_prefix_workspace_bytes(int32_t B, int32_t hq, const DecodePlan &plan,
                                      int32_t max_prefix_len);
 hipError_t launch_decode_shared_prefix(const uint16_t *q, const PagedKV &kv,

@@ -51,12 +51,15 @@ def run_shared(q, k, v, bt, lens, gs, prefix, dev, max_prefix=None):
 
 
 @pytest.mark.parametrize("Hq,Hkv,sizes", [
-    (32, 8, [8, 8, 8]),        # G = 4: 8 rollouts fill 32 columns (two tiles)
-    (16, 2, [3, 1, 8, 5]),     # G = 8: groups of 8 split into two 4-row chunks
-    (16, 1, [2, 3]),           # G = 16: two rows per chunk
+    (32, 8, [8, 8, 8]),        # G = 4: a 16-column tile holds 4 rows, two chunks a group
+    (16, 2, [3, 1, 8, 5]),     # G = 8: groups of up to 8 split into 2-row chunks
+    (16, 1, [2, 3]),           # G = 16: one row per chunk
     (8, 8, [16, 4]),           # G = 1: one tile holds 16 rows
     (32, 1, [3, 2]),           # G = 32: one row per chunk, two tiles (suffixes too)
     (24, 1, [2, 1]),           # G = 24: two tiles, the second partly empty
+    # G = 4, nine ragged groups: the prefix items fill several grid planes, the
+    # last one partly
+    (32, 8, [5, 8, 3, 1, 7, 2, 8, 4, 6]),
 ])
 def test_shared_prefix_decode_vs_oracle(device, Hq, Hkv, sizes):
     say(f"shared-prefix decode Hq={Hq} Hkv={Hkv} groups={sizes}")
