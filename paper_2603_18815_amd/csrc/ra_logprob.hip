@@ -23,6 +23,9 @@
 // grid is mapped so that the token blocks of one vocabulary chunk run on one
 // XCD and re-read the chunk from that XCD's L2.
 //
+// From N = 512 on, the partials come from the 256 x 256 tiled kernel further
+// down (256-row chunks) instead.
+//
 // Combine kernel: one wave per token merges its partials in chunk order:
 // M = max_c m_c, L = sum_c l_c 2^(m_c - M), lse = (M + log2 L) ln 2.
 //
@@ -47,6 +50,11 @@ constexpr int kMaxTiles = 4;                  // 32-token tiles per workgroup (l
 constexpr int kDimStep = 64;                  // dims per loop step (4 products)
 constexpr int kXcds = 8;                      // XCDs of an MI355X
 constexpr int kHPitch = kDimStep + 8;         // LDS row pitch of the h slice (elements)
+constexpr int kTileMinN = 512;                // batches from this size use the 256 x 256 tiles
+constexpr int kPackRows = 256;                // the packed copy covers V rounded up to this
+// s_waitcnt immediates: vmcnt(8) / vmcnt(0), export and LDS counters not waited on
+constexpr int kWaitVm8 = 0x0F78;
+constexpr int kWaitVm0 = 0x0F70;
 
 struct LogprobArgs {
   const uint16_t *h;
@@ -224,6 +232,214 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   }
 }
 
+// ---- large batches: LDS-tiled products, 256 vocabulary rows x 256 tokens ----
+//
+// At N >= kTileMinN one workgroup of 8 waves (one per compute unit) owns a
+// 256 x 256 tile of logits. Each compute unit then loads 64 bytes of W and h
+// per 128 x 32 multiply-adds of a product, half of what the 128 x 128 tiles
+// above load; those are bound by how fast the L2 delivers operands to the
+// compute units, not by the matrix cores. The loop walks D in steps of 32
+// dims through a ring of 4 LDS stages (16 KB of W and 16 KB of h each),
+// refilled three steps ahead by direct global-to-LDS loads
+// (global_load_lds_dwordx4, no register staging); the four refill loads of a
+// step are spread between its products. Wave w computes rows 64 (w % 4) ..
+// + 63 (two 32-row tiles) against tokens 128 (w / 4) .. + 127 (four 32-token
+// tiles): 16 products per step from 12 LDS operand reads.
+//
+// Stage layout: row r of a 256-row region holds its 32 dims as four 16-byte
+// chunks, logical chunk c at slot c ^ ((r / 4) % 4), so that 16 lanes reading
+// 16 rows at one logical chunk hit 16 distinct bank groups. A load
+// instruction fills 16 rows: lane l fetches row 16 j + l / 4, the logical
+// chunk stored at slot l % 4. The 32 dims of a step split over the two
+// products as lanes 0-31 dims 8 u + 0..7 and lanes 32-63 dims 16 + 8 u + 0..7
+// (logical chunk 2 half + u).
+constexpr int kTileRows = 256;        // vocabulary rows and tokens per workgroup
+constexpr int kTileWaves = 8;
+constexpr int kTileThreads = kTileWaves * kWave;
+constexpr int kTileDims = 32;         // dims per step
+constexpr int kTileStages = 4;
+constexpr int kTileElems = kTileRows * kTileDims;   // one region of a stage (16 KB)
+constexpr int kTileLoads = kTileRows / 16 / kTileWaves;   // load instructions per wave and region
+
+// Direct global-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS
+// address `lds` + 16 l (lds wave-uniform). Written out rather than through the
+// compiler builtin, which makes the compiler wait for every such load before
+// any LDS read (it cannot tell the ring's stages apart); the kernel counts
+// its own loads. M0 (the LDS base register) is restored before the statement
+// ends.
+__device__ __forceinline__ uint32_t lds_address(const uint16_t *p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void *)p;
+}
+__device__ __forceinline__ void load_lds16(const uint16_t *g, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(g)
+      : "memory");
+}
+
+template <bool kPacked>
+__global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
+  const int id = blockIdx.x;
+  const int xcd = id % kXcds, slot = id / kXcds;
+  const int chunk = (slot / a.token_blocks) * kXcds + xcd;
+  const int tblock = slot - (slot / a.token_blocks) * a.token_blocks;
+  if (chunk >= a.chunks) return;
+
+  __shared__ __attribute__((aligned(1024))) uint16_t sA[kTileStages][kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sB[kTileStages][kTileElems];
+  __shared__ float s_m[4][kTileRows];
+  __shared__ float s_l[4][kTileRows];
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int v0 = chunk * kTileRows, t0 = tblock * kTileRows;
+
+  // ---- loads: instructions kTileLoads * wave + k of each region ----
+  const uint16_t *ga[kTileLoads], *gb[kTileLoads];
+#pragma unroll
+  for (int k = 0; k < kTileLoads; ++k) {
+    const int r = 16 * (kTileLoads * wave + k) + lane / 4;
+    const int lc = (lane % 4) ^ ((r >> 2) & 3);   // logical chunk of my slot
+    const int v = v0 + r;
+    // packed: 16-byte unit ((tile * D/64 + s / 2) * 4 + lc) * 64 + 32 (s % 2) + v % 32
+    // (the part that depends on the step s is added per step)
+    ga[k] = kPacked ? a.W + (((size_t)(v / 32) * (a.D / 64)) * 4 + lc) * kWave * 8 + (v % 32) * 8
+                    : a.W + (size_t)min(v, a.V - 1) * a.D + 8 * lc;
+    gb[k] = a.h + (size_t)min(t0 + r, a.N - 1) * a.D + 8 * lc;
+  }
+  const int nsteps = a.D / kTileDims;
+  const int last = nsteps - 1;
+  const uint32_t my_block = (uint32_t)(kTileLoads * wave) * 1024u;
+  // offsets (elements) of step s in W and h; steps past the last repeat it
+  // (branch-free, so that every step issues the same number of loads)
+  auto w_off = [&](int s) __attribute__((always_inline)) {
+    return kPacked ? (size_t)(s >> 1) * 4 * kWave * 8 + (s & 1) * 32 * 8 : (size_t)s * kTileDims;
+  };
+  auto load = [&](int st, int s, int d) __attribute__((always_inline)) {
+    const int k = d >> 1;
+    if (d & 1)
+      load_lds16(gb[k] + (size_t)s * kTileDims, lds_address(sB[st]) + my_block + 1024u * k);
+    else
+      load_lds16(ga[k] + w_off(s), lds_address(sA[st]) + my_block + 1024u * k);
+  };
+  constexpr int kLoadsPerStep = 2 * kTileLoads;
+
+  // ---- products ----
+  const int col = lane & 31, half = lane >> 5;
+  const int wv = wave & 3, wt = wave >> 2;
+  const int swz = (col >> 2) & 3;   // slot swizzle of every operand row (rows differ from col by multiples of 32)
+  const int rowA = (64 * wv + col) * kTileDims, rowB = (128 * wt + col) * kTileDims;
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+  auto lds16 = [](const uint16_t *p) __attribute__((always_inline)) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+  };
+  // Step s on stage st: wait until my loads for it have landed (the ones for
+  // the next two steps may still be in flight), barrier (everyone's have, and
+  // everyone is done reading the stage used last step), then the products,
+  // with the loads of step s + 3 into that freed stage between them.
+  auto step = [&](int st, int s) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(kWaitVm8);
+    __builtin_amdgcn_s_barrier();
+    const uint16_t *A = sA[st], *B = sB[st];
+    const int rs = min(s + kTileStages - 1, last), rst = (st + kTileStages - 1) % kTileStages;
+    bf16x8 av[2][2], bv[2][4];
+    auto read = [&](int u, bf16x8 *pa, bf16x8 *pb) __attribute__((always_inline)) {
+      const int c = 8 * ((2 * half + u) ^ swz);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) pa[i] = lds16(A + rowA + c + 32 * kTileDims * i);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pb[j] = lds16(B + rowB + c + 32 * kTileDims * j);
+    };
+    read(0, av[0], bv[0]);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (u == 0) read(1, av[1], bv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          acc[i][j] = mfma32x32x16(av[u][i], bv[u][j], acc[i][j]);
+          const int p = 8 * u + 4 * i + j;   // product index in the step
+          if ((p + 1) % (16 / kLoadsPerStep) == 0) {
+            __builtin_amdgcn_sched_barrier(0);
+            load(rst, rs, p / (16 / kLoadsPerStep));
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < kTileStages - 1; ++k)
+#pragma unroll
+    for (int d = 0; d < kLoadsPerStep; ++d) load(k, min(k, last), d);
+  for (int s = 0; s < nsteps; s += kTileStages) {
+#pragma unroll
+    for (int k = 0; k < kTileStages; ++k)
+      if (s + k < nsteps) step(k, s + k);
+  }
+  // the last loads (repeats of the last step) must land before the
+  // workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+
+  // ---- logits -> (max, sum) per token over this wave's 64 rows ----
+  // Lane l holds, for token t0 + 128 wt + 32 j + col, the logits of rows
+  // v0 + 64 wv + 32 i + 8 (r / 4) + 4 half + r % 4, r = 0..15.
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int tc = 128 * wt + 32 * j + col, t = t0 + tc;
+    const int target = t < a.N ? a.targets[t] : -1;
+    float y[2][16];
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = v0 + 64 * wv + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
+        y[i][r] = v < a.V ? acc[i][j][r] * a.scale_log2 : -INFINITY;
+        m = fmaxf(m, y[i][r]);
+        if (v == target) a.tgt[t] = acc[i][j][r] * a.scale;
+      }
+    m = pair_max(m);
+    const float m_use = m == -INFINITY ? 0.f : m;
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sum += fast_exp2(y[i][r] - m_use);
+    sum = pair_sum(sum);
+    if (half == 0) {
+      s_m[wv][tc] = m;
+      s_l[wv][tc] = sum;
+    }
+  }
+  __syncthreads();
+  // merge the four row quarters: one thread per token of the tile
+  const int c = threadIdx.x;
+  if (c < kTileRows && t0 + c < a.N) {
+    float M = s_m[0][c];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) M = fmaxf(M, s_m[w][c]);
+    const float M_use = M == -INFINITY ? 0.f : M;
+    float L = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) L += s_l[w][c] * fast_exp2(s_m[w][c] - M_use);
+    const size_t part = (size_t)(t0 + c) * a.chunks + chunk;
+    a.ws_m[part] = M;
+    a.ws_l[part] = L;
+  }
+}
+
 // Packed copy of W: 16-byte unit i = ((tile * D/64 + s) * 4 + u) * 64 + lane
 // holds W[32 tile + lane % 32][64 s + 32 (lane / 32) + 8 u + 0..7] (zeros for
 // rows past V).
@@ -270,12 +486,15 @@ __global__ __launch_bounds__(kLpThreads) void logprob_combine_kernel(LogprobArgs
 
 }  // namespace
 
-int32_t logprob_chunks(int32_t V) { return (V + kVocabChunk - 1) / kVocabChunk; }
+int32_t logprob_chunks(int32_t N, int32_t V) {
+  const int rows = N >= kTileMinN ? kTileRows : kVocabChunk;
+  return (V + rows - 1) / rows;
+}
 
 // The packed copy covers every row a workgroup reads: V rounded up to whole
-// 128-row chunks.
+// 256-row chunks (so to whole 128-row chunks too).
 size_t logprob_packed_bytes(int32_t V, int32_t D) {
-  return (size_t)logprob_chunks(V) * kVocabChunk * D * sizeof(uint16_t);
+  return (size_t)((V + kPackRows - 1) / kPackRows) * kPackRows * D * sizeof(uint16_t);
 }
 
 hipError_t launch_logprob_pack(const uint16_t *W, int32_t V, int32_t D, uint16_t *Wp,
@@ -288,16 +507,18 @@ hipError_t launch_logprob_pack(const uint16_t *W, int32_t V, int32_t D, uint16_t
 }
 
 size_t logprob_workspace_bytes(int32_t N, int32_t V) {
-  return ((size_t)N * logprob_chunks(V) * 2 + (size_t)N) * sizeof(float);
+  return ((size_t)N * logprob_chunks(N, V) * 2 + (size_t)N) * sizeof(float);
 }
 
 namespace {
 int logprob_tiles(int32_t N) { return N <= 64 ? 2 : kMaxTiles; }
+// tokens per workgroup
+int logprob_token_block(int32_t N) { return N >= kTileMinN ? kTileRows : 32 * logprob_tiles(N); }
 }  // namespace
 
 int64_t logprob_grid(int32_t N, int32_t V) {
-  const int64_t chunks_pad = (logprob_chunks(V) + kXcds - 1) / kXcds * kXcds;
-  const int block = 32 * logprob_tiles(N);
+  const int64_t chunks_pad = (logprob_chunks(N, V) + kXcds - 1) / kXcds * kXcds;
+  const int block = logprob_token_block(N);
   return chunks_pad * ((N + block - 1) / block);
 }
 
@@ -311,16 +532,20 @@ hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *t
   a.N = N;
   a.V = V;
   a.D = D;
-  a.chunks = logprob_chunks(V);
+  a.chunks = logprob_chunks(N, V);
   const int tiles = logprob_tiles(N);
-  a.token_blocks = (N + 32 * tiles - 1) / (32 * tiles);
+  a.token_blocks = (N + logprob_token_block(N) - 1) / logprob_token_block(N);
   a.ws_m = static_cast<float *>(workspace);
   a.ws_l = a.ws_m + (size_t)N * a.chunks;
   a.tgt = a.ws_l + (size_t)N * a.chunks;
   a.scale = scale;
   a.scale_log2 = scale * kLog2e;
   const dim3 grid((unsigned)logprob_grid(N, V));
-  if (tiles == 2 && packed)
+  if (N >= kTileMinN && packed)
+    hipLaunchKernelGGL(logprob_tile_kernel<true>, grid, dim3(kTileThreads), 0, stream, a);
+  else if (N >= kTileMinN)
+    hipLaunchKernelGGL(logprob_tile_kernel<false>, grid, dim3(kTileThreads), 0, stream, a);
+  else if (tiles == 2 && packed)
     hipLaunchKernelGGL((logprob_partial_kernel<2, true>), grid, dim3(kLpThreads), 0, stream, a);
   else if (tiles == 2)
     hipLaunchKernelGGL((logprob_partial_kernel<2, false>), grid, dim3(kLpThreads), 0, stream, a);
