@@ -173,3 +173,48 @@ def test_fp8_rope_logprob_step_replays_in_a_graph(device):
                                   "rope append_write lse", "fp8 mixed decode",
                                   "fp8 mixed append", "logprob", "logprob lse",
                                   "packed logprob", "packed logprob lse"), (k_pool, v_pool))
+
+
+def test_shared_prefix_and_large_batch_logprob_replay_in_a_graph(device):
+    """Shared-prefix decode (prefix and row items in one launch) and the
+    log-probabilities of a batch large enough for the tiled LM-head kernel
+    (N >= 512), captured together."""
+    rng = np.random.default_rng(47)
+    sizes, Hq, Hkv = [5, 8, 3], 32, 8
+    pre = np.array([40, 9, 70], np.int64) * 16
+    suffix = rng.integers(1, 900, size=sum(sizes))
+    lay = synth.shared_prefix_layout(rng, sizes, pre, suffix)
+    say(f"graph shared prefix groups={sizes} + logprob N=600")
+    gen = synth.value_generator(47, device)
+    k_pool = synth.randn_bf16((lay.num_pages, Hkv, 16, 128), gen, device)
+    v_pool = synth.randn_bf16((lay.num_pages, Hkv, 128, 16), gen, device)
+    q = synth.randn_bf16((len(suffix), Hq, 128), gen, device)
+    kv = ra.PagedKV(k_pool, v_pool, i32(lay.block_table, device))
+    lens = lay.row_tokens.astype(np.int32)
+    gs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    lens_t, gs_t, pre_t = i32(lens, device), i32(gs, device), i32(pre, device)
+    B, mk, mg, mp = len(suffix), int(lens.max()), max(sizes), int(pre.max())
+    V, N, D = 1000, 600, 128
+    W = synth.randn_bf16((V, D), gen, device)
+    h = synth.randn_bf16((N, D), gen, device)
+    targets = i32(np.random.default_rng(48).integers(0, V, N), device)
+    Wp = ra.token_logprob_pack_weight(W)
+    f32 = dict(dtype=torch.float32, device=device)
+    u8 = dict(dtype=torch.uint8, device=device)
+    out, lse = torch.empty((B, Hq, 128), **f32), torch.empty((B, Hq), **f32)
+    ws = torch.empty(ra.decode_shared_prefix_workspace_size(B, Hq, Hkv, mk, mp), **u8)
+    lp, lp_lse = torch.empty((N,), **f32), torch.empty((N,), **f32)
+    lpp, lpp_lse = torch.empty((N,), **f32), torch.empty((N,), **f32)
+    ws_l = torch.empty(ra.token_logprob_workspace_size(N, V), **u8)
+    ws_p = torch.empty(ra.token_logprob_workspace_size(N, V), **u8)
+
+    def step():
+        ra.decode_shared_prefix(q, kv, lens_t, gs_t, pre_t, mg, mp, mk, SCALE, out=out, lse=lse,
+                                workspace=ws)
+        ra.token_logprob(h, W, targets, out=lp, lse=lp_lse, workspace=ws_l)
+        ra.token_logprob_packed(h, Wp, V, targets, out=lpp, lse=lpp_lse, workspace=ws_p)
+
+    replay_and_check(step, (out, lse, lp, lp_lse, lpp, lpp_lse),
+                     ("shared-prefix decode", "shared-prefix lse", "logprob N=600",
+                      "logprob N=600 lse", "packed logprob N=600", "packed logprob N=600 lse"),
+                     (k_pool, v_pool))
