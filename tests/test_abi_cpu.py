@@ -104,6 +104,8 @@ def test_shared_prefix_decode_validation(lib):
     assert call(ws=None) == _lib.RA_ERR_WORKSPACE
     big = dict(B=65535, ng=65535, mgr=2, max_kv_len=64)
     assert call(**big) == _lib.RA_ERR_UNSUPPORTED    # grid of groups x rows too large
+    # the row planes alone fit (65,535), the prefix items' planes push the grid past it
+    assert call(B=65535, ng=1, mgr=65535, mpl=16, max_kv_len=32) == _lib.RA_ERR_UNSUPPORTED
     assert call(B=0) == _lib.RA_OK
     f = lib.rollout_attn_decode_shared_prefix_workspace_size
     plain = lib.rollout_attn_decode_workspace_size(64, 32, 8, 32768)
