@@ -177,8 +177,11 @@ int rollout_attn_decode_noalloc(const void *q, const ra_paged_kv *kv, const int3
  * (Sec. 4 generates several rollouts per task instance; Sec. 3.3.2 keeps all
  * calls of a task on one backend so that its cached prefix is reused). The
  * result is that of rollout_attn_decode on the same rows (up to rounding: the
- * keys are split differently); the shared keys are read once per group (per
- * 32 / (Hq / Hkv) rows of a group) instead of once per row.
+ * keys are split differently); the shared keys are read once for up to
+ * 16 / (Hq / Hkv) rows of a group (one row per read for groups of more than
+ * 16 query heads) instead of once per row, and the reads of one group's
+ * chunks of rows are scheduled together so that the later ones mostly hit
+ * the cache.
  * For group i, rows group_start[i] .. group_start[i+1]-1 attend their first P_i
  * keys together, P_i = min(prefix_len[i], shortest kv_lens of the group)
  * rounded down to a multiple of 32, read through the block table of the
@@ -198,8 +201,10 @@ int rollout_attn_decode_noalloc(const void *q, const ra_paged_kv *kv, const int3
  *                   max_kv_len, max_prefix_len) bytes (contents on entry ignored)
  * Errors: as rollout_attn_decode; RA_ERR_SHAPE also for num_groups == 0 or
  *         max_group_rows == 0 with B > 0, max_group_rows > B, num_groups > B,
- *         max_prefix_len > max_kv_len; RA_ERR_UNSUPPORTED when num_groups *
- *         max_group_rows (or the prefix grid) exceeds 65535.
+ *         max_prefix_len > max_kv_len; RA_ERR_UNSUPPORTED when the launch grid
+ *         needs more than 65535 planes: num_groups * max_group_rows row planes
+ *         plus ceil(num_groups * chunks * prefix splits / splits) prefix planes,
+ *         chunks = ceil(max_group_rows / rows per chunk).
  */
 size_t rollout_attn_decode_shared_prefix_workspace_size(int32_t B, int32_t Hq, int32_t Hkv,
                                                         int32_t max_kv_len,
