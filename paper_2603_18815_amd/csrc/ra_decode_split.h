@@ -187,6 +187,15 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
     const int id0 = clamp_page(bt[pg], a.num_pages);
     const int id1 = pg + 1 < row_pages ? clamp_page(bt[pg + 1], a.num_pages) : id0;
 
+    // V loads: each instruction takes whole 128-byte lines (512 contiguous
+    // bytes per page), read once, so they are marked nontemporal; that keeps
+    // the streamed V from displacing the K lines, each of which two
+    // instructions read half at a time (K stays an ordinary load). Prefix
+    // items keep ordinary loads: the chunks of a group re-read their pages
+    // from the cache.
+    auto load_v = [](const void *p) __attribute__((always_inline)) {
+      return kPrefix ? *reinterpret_cast<const u32x4 *>(p) : load_stream_u32x4(p);
+    };
     bf16x8 ka[2][4];
     bf16x8 va[8];
     if constexpr (kFp8) {
@@ -211,7 +220,7 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
       const int vh = (lane >> 4) & 1;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const u32x4 w = *reinterpret_cast<const u32x4 *>(vb + (16 * (2 * j + vh) + col) * kPage);
+        const u32x4 w = load_v(vb + (16 * (2 * j + vh) + col) * kPage);
         const auto s0 = __builtin_amdgcn_permlane16_swap(w[0], w[2], false, false);
         const auto s1 = __builtin_amdgcn_permlane16_swap(w[1], w[3], false, false);
         va[2 * j] = fp8x8_to_bf16x8(u32x2{s0[0], s1[0]});
@@ -229,7 +238,7 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
           a.v_pool + ((size_t)(sv_sel ? id1 : id0) * a.hkv + g) * head_stride;
 #pragma unroll
       for (int mt = 0; mt < 8; ++mt)
-        va[mt] = load_bf16x8(vb + (16 * mt + col) * kPage + sv_slot);
+        va[mt] = __builtin_bit_cast(bf16x8, load_v(vb + (16 * mt + col) * kPage + sv_slot));
     }
 
     // Keys at or past t1 are not attended: their scores become -inf and

@@ -24,6 +24,12 @@ __device__ __forceinline__ u32x4 load_u32x4(const uint16_t *p) {
   return *reinterpret_cast<const u32x4 *>(p);
 }
 
+// 16-byte global load marked nontemporal (the load's nt bit): for data read
+// once, whose cache lines are each taken whole by one load instruction.
+__device__ __forceinline__ u32x4 load_stream_u32x4(const void *p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
 __device__ __forceinline__ void store_u32x4(uint16_t *p, u32x4 v) {
   *reinterpret_cast<u32x4 *>(p) = v;
 }
