@@ -49,12 +49,13 @@ int ra_mb_mfma_bf16(const void *operands, int32_t blocks, int32_t iters, float *
 int ra_mb_lds_read(int32_t blocks, int32_t iters, uint32_t *sink, int64_t *clocks,
                    hipStream_t stream);
 
-/* Reads `bytes` (a multiple of 4096) from src once, 16 bytes per lane, each
- * workgroup of 256 threads one 4 KiB block per step. With order == NULL the
- * blocks are read in address order; otherwise step j reads block order[j]
- * (int32 [bytes / 4096], device memory, values clamped to the buffer), the
- * access pattern of a paged cache with shuffled pages. sink: uint32
- * [blocks * 256]. */
+/* Reads `bytes` (a multiple of 4096) from src once, 16 bytes per lane: each
+ * workgroup of 256 threads reads four 4 KiB blocks per round (four loads per
+ * lane in flight), the workgroups of a round taking consecutive block numbers.
+ * With order == NULL block number j is block j (address order); otherwise it
+ * is block order[j] (int32 [bytes / 4096], device memory, values clamped to
+ * the buffer), the access pattern of a paged cache with shuffled pages.
+ * sink: uint32 [blocks * 256]. */
 int ra_mb_stream_read(const void *src, int64_t bytes, const int32_t *order, int32_t blocks,
                       uint32_t *sink, hipStream_t stream);
 

@@ -85,30 +85,57 @@ __global__ __launch_bounds__(RA_MB_LDS_THREADS) void lds_kernel(int iters, uint3
 constexpr int kStreamThreads = 256;
 constexpr int kBlockWords = 4096 / 16;   // 16-byte words per 4 KiB block
 
+constexpr int kStreamLoads = 4;            // 16-byte loads per lane in flight per round
+
+// Block j of the pass: j itself, or order[j] clamped into the buffer.
+template <bool kPaged>
+__device__ __forceinline__ int64_t block_of(const int32_t *order, int64_t j, int64_t nblk) {
+  if constexpr (kPaged)
+    return min(max((int64_t)order[j], (int64_t)0), nblk - 1);
+  else
+    return j;
+}
+
+// Round r of a workgroup reads blocks r * gridDim.x * kStreamLoads + k * gridDim.x
+// + blockIdx.x, k < kStreamLoads, one 16-byte word per lane of each: four loads
+// per lane in flight. A paged pass requests the next round's block numbers
+// after this round's data, so their latency hides under it, and waits for the
+// data only (the loads return in order), never for the numbers.
+template <bool kPaged>
 __global__ __launch_bounds__(kStreamThreads) void stream_kernel(const u32x4 *src, int64_t nblk,
                                                                 const int32_t *order,
                                                                 uint32_t *sink) {
   const int tid = threadIdx.x;
-  u32x4 acc0 = {}, acc1 = {};
-  int64_t j = blockIdx.x;
-  const int64_t step = gridDim.x;
-  // two blocks per round, so that two 16-byte loads per lane are in flight
-  for (; j + step < nblk; j += 2 * step) {
-    int64_t b0 = j, b1 = j + step;
-    if (order) {
-      b0 = min(max((int64_t)order[b0], (int64_t)0), nblk - 1);
-      b1 = min(max((int64_t)order[b1], (int64_t)0), nblk - 1);
-    }
-    acc0 ^= __builtin_nontemporal_load(&src[b0 * kBlockWords + tid]);
-    acc1 ^= __builtin_nontemporal_load(&src[b1 * kBlockWords + tid]);
+  const int64_t step = gridDim.x, per_round = step * kStreamLoads;
+  const int64_t full = nblk / per_round * per_round;   // blocks in whole rounds
+  u32x4 acc[kStreamLoads];
+#pragma unroll
+  for (int k = 0; k < kStreamLoads; ++k) acc[k] = u32x4{0u, 0u, 0u, 0u};
+  int64_t j0 = blockIdx.x;
+  int64_t blk[kStreamLoads];
+  if (j0 < full) {
+#pragma unroll
+    for (int k = 0; k < kStreamLoads; ++k) blk[k] = block_of<kPaged>(order, j0 + k * step, nblk);
   }
-  if (j < nblk) {
-    int64_t b0 = j;
-    if (order) b0 = min(max((int64_t)order[b0], (int64_t)0), nblk - 1);
-    acc0 ^= src[b0 * kBlockWords + tid];
+  for (; j0 < full; j0 += per_round) {
+    u32x4 v[kStreamLoads];
+#pragma unroll
+    for (int k = 0; k < kStreamLoads; ++k)
+      v[k] = __builtin_nontemporal_load(&src[blk[k] * kBlockWords + tid]);
+    __builtin_amdgcn_sched_barrier(0);   // all four issued before any use
+    // the next round's blocks (this round's again after the last one: in
+    // range, and no branch between the loads and their use)
+    const int64_t jn = j0 + per_round < full ? j0 + per_round : j0;
+#pragma unroll
+    for (int k = 0; k < kStreamLoads; ++k) blk[k] = block_of<kPaged>(order, jn + k * step, nblk);
+#pragma unroll
+    for (int k = 0; k < kStreamLoads; ++k) acc[k] ^= v[k];
   }
-  const u32x4 acc = acc0 ^ acc1;
-  sink[(size_t)blockIdx.x * kStreamThreads + tid] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+  for (int64_t j = full + blockIdx.x; j < nblk; j += step)
+    acc[0] ^= src[block_of<kPaged>(order, j, nblk) * kBlockWords + tid];
+#pragma unroll
+  for (int k = 1; k < kStreamLoads; ++k) acc[0] ^= acc[k];
+  sink[(size_t)blockIdx.x * kStreamThreads + tid] = acc[0][0] ^ acc[0][1] ^ acc[0][2] ^ acc[0][3];
 }
 
 int launched() { return hipGetLastError() == hipSuccess ? 0 : 5; }
@@ -139,8 +166,12 @@ int ra_mb_stream_read(const void *src, int64_t bytes, const int32_t *order, int3
                       uint32_t *sink, hipStream_t stream) {
   if (!src || !sink) return 1;
   if (bytes <= 0 || bytes % 4096 != 0 || blocks <= 0) return 2;
-  hipLaunchKernelGGL(stream_kernel, dim3(blocks), dim3(kStreamThreads), 0, stream,
-                     static_cast<const u32x4 *>(src), bytes / 4096, order, sink);
+  if (order)
+    hipLaunchKernelGGL(stream_kernel<true>, dim3(blocks), dim3(kStreamThreads), 0, stream,
+                       static_cast<const u32x4 *>(src), bytes / 4096, order, sink);
+  else
+    hipLaunchKernelGGL(stream_kernel<false>, dim3(blocks), dim3(kStreamThreads), 0, stream,
+                       static_cast<const u32x4 *>(src), bytes / 4096, order, sink);
   return launched();
 }
 
