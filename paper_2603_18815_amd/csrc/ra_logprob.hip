@@ -134,11 +134,18 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
 #pragma unroll
     for (int i = 0; i < kHChunks; ++i) store_u32x4(&s_h[buf][hdst[i]], src[i]);
   };
+  // With one token block (kTiles == 2: N <= 64) no other workgroup reads this
+  // chunk of W, and a packed W load takes 1 KB contiguous (whole cache lines):
+  // those loads are marked nontemporal. Row-major loads take each line 32
+  // bytes at a time over four instructions and stay ordinary.
+  constexpr bool kStreamW = kPacked && kTiles == 2;
   bf16x8 w0[4], w1[4], w2[4], w3[4];
   auto w_load = [&](bf16x8 *dst, int s) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      dst[u] = load_bf16x8(kPacked ? wp + (size_t)(4 * s + u) * 8 * kWave : wp + s * kDimStep + 8 * u);
+      dst[u] = kStreamW ? __builtin_bit_cast(bf16x8, load_stream_u32x4(wp + (size_t)(4 * s + u) * 8 * kWave))
+                        : load_bf16x8(kPacked ? wp + (size_t)(4 * s + u) * 8 * kWave
+                                              : wp + s * kDimStep + 8 * u);
   };
   const int nsteps = a.D / kDimStep;
   const int last = nsteps - 1;
