@@ -289,6 +289,14 @@ def achievable_leg(dev):
         g, per_cu = max((mb.stream_read(4 << 30, paged, k * cus), k) for k in (2, 3, 4, 8))
         res[name] = {"GB_s": round(g, 1), "frac_of_published_peak": round(g / HBM_PEAK_GBS, 4),
                      "workgroups_per_CU": per_cu}
+    # the same pass in shuffled 1, 2 and 4 KiB blocks (the size of a 16-token page of one
+    # KV head with head dim 128 in fp8 / bf16 is 2 / 4 KiB)
+    src = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    res["hbm_read_shuffled_blocks_GB_s"] = {
+        f"{kb // 1024}KiB": round(max(mb.block_read(src, kb, k * cus) for k in (2, 3, 4)), 1)
+        for kb in (1024, 2048, 4096)}
+    del src
     torch.cuda.empty_cache()
     return res
 

@@ -59,6 +59,16 @@ int ra_mb_lds_read(int32_t blocks, int32_t iters, uint32_t *sink, int64_t *clock
 int ra_mb_stream_read(const void *src, int64_t bytes, const int32_t *order, int32_t blocks,
                       uint32_t *sink, hipStream_t stream);
 
+/* Reads `bytes` from src once in shuffled blocks of block_bytes (1024, 2048 or
+ * 4096; bytes / block_bytes a power of two, at least 16): block j of the pass
+ * is block mix(j) of src for a fixed bijection mix (no block numbers are read
+ * from memory), 16 bytes per lane, four loads per lane in flight, one load
+ * instruction of a 256-thread workgroup taking 4096 / block_bytes blocks. The
+ * read rate of a paged pool as a function of its block size. sink: uint32
+ * [blocks * 256]. */
+int ra_mb_block_read(const void *src, int64_t bytes, int32_t block_bytes, int32_t blocks,
+                     uint32_t *sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

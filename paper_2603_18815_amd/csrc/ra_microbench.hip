@@ -138,6 +138,50 @@ __global__ __launch_bounds__(kStreamThreads) void stream_kernel(const u32x4 *src
   sink[(size_t)blockIdx.x * kStreamThreads + tid] = acc[0][0] ^ acc[0][1] ^ acc[0][2] ^ acc[0][3];
 }
 
+// A fixed bijection of [0, 2^bits) (xor-shift and odd-multiply rounds, each
+// invertible modulo 2^bits): block j of a pass reads block mix(j).
+__device__ __forceinline__ int64_t mix_block(int64_t j, int bits) {
+  const uint64_t mask = (bits >= 64) ? ~0ull : ((1ull << bits) - 1ull);
+  const int sh = (bits + 1) / 2;
+  uint64_t h = (uint64_t)j;
+  h ^= h >> sh;
+  h = (h * 0x9E3779B97F4A7C15ull) & mask;
+  h ^= h >> sh;
+  h = (h * 0xBF58476D1CE4E5B9ull) & mask;
+  h ^= h >> sh;
+  return (int64_t)h;
+}
+
+// Shuffled blocks of kBytes bytes: one load instruction of the workgroup takes
+// 4096 / kBytes blocks (kBytes / 16 lanes each), four loads per lane in
+// flight per round, no block numbers read from memory.
+template <int kBytes>
+__global__ __launch_bounds__(kStreamThreads) void block_read_kernel(const u32x4 *src, int64_t nblk,
+                                                                    int bits, uint32_t *sink) {
+  constexpr int kWords = kBytes / 16, kPer = 4096 / kBytes;
+  const int tid = threadIdx.x, sub = tid / kWords, w = tid % kWords;
+  u32x4 acc[kStreamLoads];
+#pragma unroll
+  for (int k = 0; k < kStreamLoads; ++k) acc[k] = u32x4{0u, 0u, 0u, 0u};
+  const int64_t per_round = (int64_t)gridDim.x * kPer * kStreamLoads;
+  // nblk is a power of two of at least kPer * kStreamLoads blocks and base a
+  // multiple of that, so every j below is < nblk
+  for (int64_t base = (int64_t)blockIdx.x * kPer * kStreamLoads; base < nblk; base += per_round) {
+    u32x4 v[kStreamLoads];
+#pragma unroll
+    for (int k = 0; k < kStreamLoads; ++k) {
+      const int64_t b = mix_block(base + k * kPer + sub, bits);
+      v[k] = __builtin_nontemporal_load(&src[b * kWords + w]);
+    }
+    __builtin_amdgcn_sched_barrier(0);   // all four issued before any use
+#pragma unroll
+    for (int k = 0; k < kStreamLoads; ++k) acc[k] ^= v[k];
+  }
+#pragma unroll
+  for (int k = 1; k < kStreamLoads; ++k) acc[0] ^= acc[k];
+  sink[(size_t)blockIdx.x * kStreamThreads + tid] = acc[0][0] ^ acc[0][1] ^ acc[0][2] ^ acc[0][3];
+}
+
 int launched() { return hipGetLastError() == hipSuccess ? 0 : 5; }
 
 }  // namespace
@@ -172,6 +216,28 @@ int ra_mb_stream_read(const void *src, int64_t bytes, const int32_t *order, int3
   else
     hipLaunchKernelGGL(stream_kernel<false>, dim3(blocks), dim3(kStreamThreads), 0, stream,
                        static_cast<const u32x4 *>(src), bytes / 4096, order, sink);
+  return launched();
+}
+
+int ra_mb_block_read(const void *src, int64_t bytes, int32_t block_bytes, int32_t blocks,
+                     uint32_t *sink, hipStream_t stream) {
+  if (!src || !sink) return 1;
+  if (block_bytes != 1024 && block_bytes != 2048 && block_bytes != 4096) return 2;
+  if (bytes <= 0 || bytes % block_bytes != 0 || blocks <= 0) return 2;
+  const int64_t nblk = bytes / block_bytes;
+  if ((nblk & (nblk - 1)) != 0 || nblk < 16) return 2;
+  int bits = 0;
+  while ((int64_t(1) << bits) < nblk) ++bits;
+  const u32x4 *s = static_cast<const u32x4 *>(src);
+  if (block_bytes == 1024)
+    hipLaunchKernelGGL(block_read_kernel<1024>, dim3(blocks), dim3(kStreamThreads), 0, stream, s,
+                       nblk, bits, sink);
+  else if (block_bytes == 2048)
+    hipLaunchKernelGGL(block_read_kernel<2048>, dim3(blocks), dim3(kStreamThreads), 0, stream, s,
+                       nblk, bits, sink);
+  else
+    hipLaunchKernelGGL(block_read_kernel<4096>, dim3(blocks), dim3(kStreamThreads), 0, stream, s,
+                       nblk, bits, sink);
   return launched();
 }
 

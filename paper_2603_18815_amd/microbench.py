@@ -10,7 +10,7 @@ import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libra_microbench.so")
-EXPORTS = ("ra_mb_mfma_bf16", "ra_mb_lds_read", "ra_mb_stream_read")
+EXPORTS = ("ra_mb_mfma_bf16", "ra_mb_lds_read", "ra_mb_stream_read", "ra_mb_block_read")
 MFMA_THREADS = 256
 MFMA_OPERANDS = MFMA_THREADS * 64
 LDS_THREADS = 512
@@ -27,6 +27,7 @@ def load() -> ctypes.CDLL:
         lib.ra_mb_mfma_bf16.argtypes = [vp, i32, i32, vp, vp, vp]
         lib.ra_mb_lds_read.argtypes = [i32, i32, vp, vp, vp]
         lib.ra_mb_stream_read.argtypes = [vp, i64, vp, i32, vp, vp]
+        lib.ra_mb_block_read.argtypes = [vp, i64, i32, i32, vp, vp]
         for f in EXPORTS:
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
@@ -126,3 +127,22 @@ def stream_read(nbytes: int, paged: bool, blocks: int, seed: int = 0, reps: int 
     best = min(ms)
     extra = 0 if order is None else order.numel() * 4
     return (nbytes + extra) / (best * 1e-3) / 1e9
+
+
+def block_read(src: torch.Tensor, block_bytes: int, blocks: int, reps: int = 5):
+    """HBM read rate (GB/s) of one pass over src (uint8, device; its size a power-of-two
+    multiple of block_bytes) in shuffled blocks of block_bytes (1, 2 or 4 KiB)."""
+    lib = load()
+    sink = torch.empty(blocks * 256, device=src.device, dtype=torch.int32)
+    run = lambda: _check("ra_mb_block_read", lib.ra_mb_block_read(
+        src.data_ptr(), src.numel(), block_bytes, blocks, sink.data_ptr(), _stream()))
+    run()
+    ms = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    return src.numel() / (min(ms) * 1e-3) / 1e9

@@ -432,3 +432,26 @@ def test_decode_noalloc_validation(lib):
     # the Qwen3-8B decode workload (64 rows, 32 heads, up to 32768 keys) fits
     assert lib.rollout_attn_decode_workspace_size(64, 32, 8, 32768) <= \
         _lib.RA_NOALLOC_SCRATCH_BYTES
+
+
+def test_microbench_exports_and_validation():
+    """The ceiling microbenchmarks' library exports what include/ra_microbench.h
+    declares and rejects bad arguments before any HIP call."""
+    from paper_2603_18815_amd import microbench as mb
+    text = open(os.path.join(ROOT, "include", "ra_microbench.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    declared = set(re.findall(r"^\s*int\s+(\w+)\s*\(", text, flags=re.M))
+    assert declared == set(mb.EXPORTS), declared
+    lib = mb.load()
+    for n in declared:
+        assert hasattr(lib, n), n
+    assert lib.ra_mb_block_read(None, 1 << 20, 4096, 4, FAKE, None) == 1
+    assert lib.ra_mb_block_read(FAKE, 1 << 20, 3000, 4, FAKE, None) == 2   # block size
+    assert lib.ra_mb_block_read(FAKE, 3 << 20, 4096, 4, FAKE, None) == 2   # not a power of two
+    assert lib.ra_mb_block_read(FAKE, 8 * 4096, 4096, 4, FAKE, None) == 2  # under 16 blocks
+    assert lib.ra_mb_block_read(FAKE, 1 << 20, 4096, 0, FAKE, None) == 2
+    assert lib.ra_mb_stream_read(FAKE, 4095, None, 4, FAKE, None) == 2
+    assert lib.ra_mb_stream_read(None, 4096, None, 4, FAKE, None) == 1
+    assert lib.ra_mb_mfma_bf16(None, 1, 1, FAKE, FAKE, None) == 1
+    assert lib.ra_mb_mfma_bf16(FAKE, 0, 1, FAKE, FAKE, None) == 2
+    assert lib.ra_mb_lds_read(1, 0, FAKE, FAKE, None) == 2
