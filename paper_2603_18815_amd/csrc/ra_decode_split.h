@@ -130,7 +130,10 @@ __device__ __forceinline__ void decode_split(const DecodeArgs &a, int g, int spl
   }
   if (nr <= 0 || t0 >= t1) return;
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
+  // wave-uniform (an SGPR), so that the pair loop and its block-table reads
+  // run on the scalar unit instead of as vector loads that each wait for
+  // every load issued before them
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int npairs = (t1 - t0 + kPairTokens - 1) / kPairTokens;
   const int row_pages = (t1 + kPage - 1) / kPage;   // pages of row krow in use up to t1
   const int32_t *bt = a.block_table + (size_t)krow * a.bt_stride;
