@@ -402,7 +402,7 @@ int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t 
  * Packed layout: bf16, 16-byte units; unit
  *   i = ((tile * (D / 64) + s) * 4 + u) * 64 + lane
  * holds W[32 * tile + lane % 32][64 * s + 32 * (lane / 32) + 8 * u + 0..7],
- * zeros for rows at or past V; tiles cover V rounded up to a multiple of 256.
+ * zeros for rows at or past V; tiles cover V rounded up to a multiple of 384.
  *
  * token_logprob_packed_weight_size: bytes of the packed copy (0 if V <= 0,
  *   D <= 0 or D is not a multiple of 64).

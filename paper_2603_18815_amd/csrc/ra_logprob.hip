@@ -23,8 +23,8 @@
 // grid is mapped so that the token blocks of one vocabulary chunk run on one
 // XCD and re-read the chunk from that XCD's L2.
 //
-// From N = 512 on, the partials come from the 256 x 256 tiled kernel further
-// down (256-row chunks) instead.
+// From N = 512 on, the partials come from the 384 x 256 tiled kernel further
+// down (384-row chunks) instead.
 //
 // Combine kernel: one wave per token merges its partials in chunk order:
 // M = max_c m_c, L = sum_c l_c 2^(m_c - M), lse = (M + log2 L) ln 2.
@@ -50,10 +50,9 @@ constexpr int kMaxTiles = 4;                  // 32-token tiles per workgroup (l
 constexpr int kDimStep = 64;                  // dims per loop step (4 products)
 constexpr int kXcds = 8;                      // XCDs of an MI355X
 constexpr int kHPitch = kDimStep + 8;         // LDS row pitch of the h slice (elements)
-constexpr int kTileMinN = 512;                // batches from this size use the 256 x 256 tiles
-constexpr int kPackRows = 256;                // the packed copy covers V rounded up to this
-// s_waitcnt immediates: vmcnt(8) / vmcnt(0), export and LDS counters not waited on
-constexpr int kWaitVm8 = 0x0F78;
+constexpr int kTileMinN = 512;                // batches from this size use the 384 x 256 tiles
+constexpr int kPackRows = 384;                // the packed copy covers V rounded up to this
+// s_waitcnt immediates: vmcnt(0), export and LDS counters not waited on
 constexpr int kWaitVm0 = 0x0F70;
 
 struct LogprobArgs {
@@ -239,34 +238,41 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   }
 }
 
-// ---- large batches: LDS-tiled products, 256 vocabulary rows x 256 tokens ----
+// ---- large batches: LDS-tiled products, 384 vocabulary rows x 256 tokens ----
 //
 // At N >= kTileMinN one workgroup of 8 waves (one per compute unit) owns a
-// 256 x 256 tile of logits. Each compute unit then loads 64 bytes of W and h
-// per 128 x 32 multiply-adds of a product, half of what the 128 x 128 tiles
-// above load; those are bound by how fast the L2 delivers operands to the
-// compute units, not by the matrix cores. The loop walks D in steps of 32
-// dims through a ring of 4 LDS stages (16 KB of W and 16 KB of h each),
-// refilled three steps ahead by direct global-to-LDS loads
-// (global_load_lds_dwordx4, no register staging); the four refill loads of a
-// step are spread between its products. Wave w computes rows 64 (w % 4) ..
-// + 63 (two 32-row tiles) against tokens 128 (w / 4) .. + 127 (four 32-token
-// tiles): 16 products per step from 12 LDS operand reads.
+// 384 x 256 tile of logits (vocabulary rows x tokens). Each compute unit then
+// loads 40 KB of W and h per 384 x 256 x 32 multiply-adds, about 19 % fewer
+// bytes per product than a 256 x 256 tile and less than half of what the 128 x 128
+// tiles above load; those are bound by how fast the L2 delivers operands to
+// the compute units, not by the matrix cores. The loop walks D in steps of 32
+// dims through a ring of 3 LDS stages (24 KB of W and 16 KB of h each),
+// refilled two steps ahead by direct global-to-LDS loads
+// (global_load_lds_dwordx4, no register staging); the five refill loads of a
+// wave and step are spread between its products. Wave w computes rows
+// 96 (w % 4) .. + 95 (three 32-row tiles) against tokens 128 (w / 4) .. + 127
+// (four 32-token tiles): 24 products per step from 14 LDS operand reads, 192
+// accumulator registers.
 //
-// Stage layout: row r of a 256-row region holds its 32 dims as four 16-byte
-// chunks, logical chunk c at slot c ^ ((r / 4) % 4), so that 16 lanes reading
-// 16 rows at one logical chunk hit 16 distinct bank groups. A load
-// instruction fills 16 rows: lane l fetches row 16 j + l / 4, the logical
-// chunk stored at slot l % 4. The 32 dims of a step split over the two
-// products as lanes 0-31 dims 8 u + 0..7 and lanes 32-63 dims 16 + 8 u + 0..7
-// (logical chunk 2 half + u).
-constexpr int kTileRows = 256;        // vocabulary rows and tokens per workgroup
+// Stage layout: row r of a region holds its 32 dims as four 16-byte chunks,
+// logical chunk c at slot c ^ ((r / 4) % 4), so that 16 lanes reading 16 rows
+// at one logical chunk hit 16 distinct bank groups. A load instruction fills
+// 16 rows: lane l fetches row 16 j + l / 4, the logical chunk stored at slot
+// l % 4. The 32 dims of a step split over the two products as lanes 0-31 dims
+// 8 u + 0..7 and lanes 32-63 dims 16 + 8 u + 0..7 (logical chunk 2 half + u).
+constexpr int kTileRows = 256;        // tokens per workgroup
+constexpr int kTileRowsA = 384;       // vocabulary rows per workgroup
 constexpr int kTileWaves = 8;
 constexpr int kTileThreads = kTileWaves * kWave;
 constexpr int kTileDims = 32;         // dims per step
-constexpr int kTileStages = 4;
-constexpr int kTileElems = kTileRows * kTileDims;   // one region of a stage (16 KB)
-constexpr int kTileLoads = kTileRows / 16 / kTileWaves;   // load instructions per wave and region
+constexpr int kTileStages = 3;
+constexpr int kTileElems = kTileRows * kTileDims;     // token region of a stage (16 KB)
+constexpr int kTileElemsA = kTileRowsA * kTileDims;   // vocabulary region (24 KB)
+constexpr int kLoadsA = kTileRowsA / 16 / kTileWaves;  // 3
+constexpr int kLoadsB = kTileRows / 16 / kTileWaves;   // 2
+// s_waitcnt vmcnt(5) (export and LDS counters not waited on): one later
+// step's loads may stay in flight
+constexpr int kWaitVm5 = 0x0F75;
 
 // Direct global-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS
 // address `lds` + 16 l (lds wave-uniform). Written out rather than through the
@@ -298,91 +304,95 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
   const int tblock = slot - (slot / a.token_blocks) * a.token_blocks;
   if (chunk >= a.chunks) return;
 
-  __shared__ __attribute__((aligned(1024))) uint16_t sA[kTileStages][kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sA[kTileStages][kTileElemsA];
   __shared__ __attribute__((aligned(1024))) uint16_t sB[kTileStages][kTileElems];
   __shared__ float s_m[4][kTileRows];
   __shared__ float s_l[4][kTileRows];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int v0 = chunk * kTileRows, t0 = tblock * kTileRows;
+  const int v0 = chunk * kTileRowsA, t0 = tblock * kTileRows;
 
-  // ---- loads: instructions kTileLoads * wave + k of each region ----
-  const uint16_t *ga[kTileLoads], *gb[kTileLoads];
+  // ---- loads: instructions kLoadsA * wave + k of the W region, kLoadsB *
+  // wave + k of the h region ----
+  const uint16_t *ga[kLoadsA], *gb[kLoadsB];
 #pragma unroll
-  for (int k = 0; k < kTileLoads; ++k) {
-    const int r = 16 * (kTileLoads * wave + k) + lane / 4;
-    const int lc = (lane % 4) ^ ((r >> 2) & 3);   // logical chunk of my slot
+  for (int k = 0; k < kLoadsA; ++k) {
+    const int r = 16 * (kLoadsA * wave + k) + lane / 4;
+    const int lc = (lane % 4) ^ ((r >> 2) & 3);
     const int v = v0 + r;
     // packed: 16-byte unit ((tile * D/64 + s / 2) * 4 + lc) * 64 + 32 (s % 2) + v % 32
     // (the part that depends on the step s is added per step)
     ga[k] = kPacked ? a.W + (((size_t)(v / 32) * (a.D / 64)) * 4 + lc) * kWave * 8 + (v % 32) * 8
                     : a.W + (size_t)min(v, a.V - 1) * a.D + 8 * lc;
+  }
+#pragma unroll
+  for (int k = 0; k < kLoadsB; ++k) {
+    const int r = 16 * (kLoadsB * wave + k) + lane / 4;
+    const int lc = (lane % 4) ^ ((r >> 2) & 3);
     gb[k] = a.h + (size_t)min(t0 + r, a.N - 1) * a.D + 8 * lc;
   }
   const int nsteps = a.D / kTileDims;
   const int last = nsteps - 1;
-  const uint32_t my_block = (uint32_t)(kTileLoads * wave) * 1024u;
+  const uint32_t blkA = (uint32_t)(kLoadsA * wave) * 1024u, blkB = (uint32_t)(kLoadsB * wave) * 1024u;
   // offsets (elements) of step s in W and h; steps past the last repeat it
   // (branch-free, so that every step issues the same number of loads)
   auto w_off = [&](int s) __attribute__((always_inline)) {
     return kPacked ? (size_t)(s >> 1) * 4 * kWave * 8 + (s & 1) * 32 * 8 : (size_t)s * kTileDims;
   };
   auto load = [&](int st, int s, int d) __attribute__((always_inline)) {
-    const int k = d >> 1;
-    if (d & 1)
-      load_lds16(gb[k] + (size_t)s * kTileDims, lds_address(sB[st]) + my_block + 1024u * k);
+    if (d < kLoadsA)
+      load_lds16(ga[d] + w_off(s), lds_address(sA[st]) + blkA + 1024u * d);
     else
-      load_lds16(ga[k] + w_off(s), lds_address(sA[st]) + my_block + 1024u * k);
+      load_lds16(gb[d - kLoadsA] + (size_t)s * kTileDims,
+                 lds_address(sB[st]) + blkB + 1024u * (d - kLoadsA));
   };
-  constexpr int kLoadsPerStep = 2 * kTileLoads;
+  constexpr int kLoadsPerStep = kLoadsA + kLoadsB;
+  // refill load d of a step goes after product kLoadAfter[d] of its 24
+  constexpr int kLoadAfter[kLoadsPerStep] = {3, 8, 13, 18, 22};
 
-  // ---- products ----
   const int col = lane & 31, half = lane >> 5;
   const int wv = wave & 3, wt = wave >> 2;
   const int swz = (col >> 2) & 3;   // slot swizzle of every operand row (rows differ from col by multiples of 32)
-  const int rowA = (64 * wv + col) * kTileDims, rowB = (128 * wt + col) * kTileDims;
-  f32x16 acc[2][4];
+  const int rowA = (96 * wv + col) * kTileDims, rowB = (128 * wt + col) * kTileDims;
+  f32x16 acc[3][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 3; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
   auto lds16 = [](const uint16_t *p) __attribute__((always_inline)) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
   };
-  // Step s on stage st: wait until my loads for it have landed (the ones for
-  // the next two steps may still be in flight), barrier (everyone's have, and
-  // everyone is done reading the stage used last step), then the products,
-  // with the loads of step s + 3 into that freed stage between them.
+  // Step s on stage st: wait until my loads for it have landed (the next
+  // step's may still be in flight), barrier (everyone's have, and everyone is
+  // done reading the stage used last step), then the products, with the
+  // loads of step s + 2 into that freed stage between them.
   auto step = [&](int st, int s) __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(kWaitVm8);
+    __builtin_amdgcn_s_waitcnt(kWaitVm5);
     __builtin_amdgcn_s_barrier();
     const uint16_t *A = sA[st], *B = sB[st];
     const int rs = min(s + kTileStages - 1, last), rst = (st + kTileStages - 1) % kTileStages;
-    bf16x8 av[2][2], bv[2][4];
-    auto read = [&](int u, bf16x8 *pa, bf16x8 *pb) __attribute__((always_inline)) {
-      const int c = 8 * ((2 * half + u) ^ swz);
-#pragma unroll
-      for (int i = 0; i < 2; ++i) pa[i] = lds16(A + rowA + c + 32 * kTileDims * i);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) pb[j] = lds16(B + rowB + c + 32 * kTileDims * j);
-    };
-    read(0, av[0], bv[0]);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      if (u == 0) read(1, av[1], bv[1]);
-      __builtin_amdgcn_sched_barrier(0);
+      const int c = 8 * ((2 * half + u) ^ swz);
+      bf16x8 av[3], bv[4];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 3; ++i) av[i] = lds16(A + rowA + c + 32 * kTileDims * i);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bv[j] = lds16(B + rowB + c + 32 * kTileDims * j);
+#pragma unroll
+      for (int i = 0; i < 3; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          acc[i][j] = mfma32x32x16(av[u][i], bv[u][j], acc[i][j]);
-          const int p = 8 * u + 4 * i + j;   // product index in the step
-          if ((p + 1) % (16 / kLoadsPerStep) == 0) {
-            __builtin_amdgcn_sched_barrier(0);
-            load(rst, rs, p / (16 / kLoadsPerStep));
-            __builtin_amdgcn_sched_barrier(0);
-          }
+          acc[i][j] = mfma32x32x16(av[i], bv[j], acc[i][j]);
+          const int p = 12 * u + 4 * i + j;   // product index in the step, 0..23
+#pragma unroll
+          for (int d = 0; d < kLoadsPerStep; ++d)
+            if (p == kLoadAfter[d]) {
+              __builtin_amdgcn_sched_barrier(0);
+              load(rst, rs, d);
+              __builtin_amdgcn_sched_barrier(0);
+            }
         }
     }
   };
@@ -399,20 +409,20 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
   // workgroup's LDS is released
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
 
-  // ---- logits -> (max, sum) per token over this wave's 64 rows ----
+  // ---- logits -> (max, sum) per token over this wave's 96 rows ----
   // Lane l holds, for token t0 + 128 wt + 32 j + col, the logits of rows
-  // v0 + 64 wv + 32 i + 8 (r / 4) + 4 half + r % 4, r = 0..15.
+  // v0 + 96 wv + 32 i + 8 (r / 4) + 4 half + r % 4, r = 0..15.
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int tc = 128 * wt + 32 * j + col, t = t0 + tc;
     const int target = t < a.N ? a.targets[t] : -1;
-    float y[2][16];
+    float y[3][16];
     float m = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 3; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int v = v0 + 64 * wv + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
+        const int v = v0 + 96 * wv + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
         y[i][r] = v < a.V ? acc[i][j][r] * a.scale_log2 : -INFINITY;
         m = fmaxf(m, y[i][r]);
         if (v == target) a.tgt[t] = acc[i][j][r] * a.scale;
@@ -421,7 +431,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     const float m_use = m == -INFINITY ? 0.f : m;
     float sum = 0.f;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 3; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) sum += fast_exp2(y[i][r] - m_use);
     sum = pair_sum(sum);
@@ -431,7 +441,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     }
   }
   __syncthreads();
-  // merge the four row quarters: one thread per token of the tile
+  // merge the four row groups: one thread per token of the tile
   const int c = threadIdx.x;
   if (c < kTileRows && t0 + c < a.N) {
     float M = s_m[0][c];
@@ -494,12 +504,12 @@ __global__ __launch_bounds__(kLpThreads) void logprob_combine_kernel(LogprobArgs
 }  // namespace
 
 int32_t logprob_chunks(int32_t N, int32_t V) {
-  const int rows = N >= kTileMinN ? kTileRows : kVocabChunk;
+  const int rows = N >= kTileMinN ? kTileRowsA : kVocabChunk;
   return (V + rows - 1) / rows;
 }
 
 // The packed copy covers every row a workgroup reads: V rounded up to whole
-// 256-row chunks (so to whole 128-row chunks too).
+// 384-row chunks (so to whole 128-row chunks too).
 size_t logprob_packed_bytes(int32_t V, int32_t D) {
   return (size_t)((V + kPackRows - 1) / kPackRows) * kPackRows * D * sizeof(uint16_t);
 }

@@ -97,7 +97,7 @@ int main(void) {
          token_logprob(fake, fake, ifake, 8, 100, 96, 1.0f, ffake, NULL, ws, sizeof ws, 0),
          RA_ERR_UNSUPPORTED);
   expect("packed weight size",
-         (int)(token_logprob_packed_weight_size(100, 128) == (size_t)256 * 128 * 2), 1);
+         (int)(token_logprob_packed_weight_size(100, 128) == (size_t)384 * 128 * 2), 1);
   expect("pack weight: small buffer",
          token_logprob_pack_weight(fake, 100, 128, fake, 16, 0), RA_ERR_WORKSPACE);
   expect("logprob packed: NULL W",

@@ -132,13 +132,13 @@ def test_token_logprob_validation(lib):
     assert f(0, 100) == 0 and f(8, 0) == 0
     assert f(64, 151936) == (64 * 1187 * 2 + 64) * 4     # 1187 chunks of 128 rows
     assert f(511, 151936) == (511 * 1187 * 2 + 511) * 4
-    assert f(512, 151936) == (512 * 594 * 2 + 512) * 4   # from N = 512: 594 chunks of 256 rows
+    assert f(512, 151936) == (512 * 396 * 2 + 512) * 4   # from N = 512: 396 chunks of 384 rows
 
 
 def test_token_logprob_packed_validation(lib):
     size = lib.token_logprob_packed_weight_size
-    assert size(151936, 4096) == 594 * 256 * 4096 * 2    # V rounded up to 256 rows
-    assert size(1, 64) == 256 * 64 * 2
+    assert size(151936, 4096) == 396 * 384 * 4096 * 2    # V rounded up to 384 rows
+    assert size(1, 64) == 384 * 64 * 2
     assert size(0, 64) == 0 and size(10, 0) == 0 and size(10, 96) == 0
 
     def pack(**kw):
@@ -150,7 +150,7 @@ def test_token_logprob_packed_validation(lib):
     assert pack(V=0) == _lib.RA_ERR_SHAPE
     assert pack(D=-64) == _lib.RA_ERR_SHAPE
     assert pack(D=96) == _lib.RA_ERR_UNSUPPORTED
-    assert pack(nbytes=256 * 128 * 2 - 1) == _lib.RA_ERR_WORKSPACE
+    assert pack(nbytes=384 * 128 * 2 - 1) == _lib.RA_ERR_WORKSPACE
 
     def call(**kw):
         d = dict(h=FAKE, W=FAKE, t=FAKE, N=8, V=100, D=128, out=FAKE, ws=FAKE, ws_bytes=1 << 30)

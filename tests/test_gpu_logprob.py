@@ -52,12 +52,12 @@ def check(lp, ls, ref_lp, ref_ls, what):
     (5, 257, 192, 0.7),      # temperature scale, vocabulary of 2 chunks + 1 row
     (1, 1, 64, 1.0),         # a single vocabulary entry: logp = 0
     (130, 4096, 256, 1.0),   # three token blocks, 32 chunks (4 per XCD)
-    # from N = 512 on: 256 x 256 tiles through the LDS ring
-    (512, 1000, 128, 0.7),   # two token blocks, a ragged last 256-row chunk
+    # from N = 512 on: 384 x 256 tiles through the LDS ring
+    (512, 1000, 128, 0.7),   # two token blocks, a ragged last 384-row chunk
     (600, 5000, 256, 1.0),   # a ragged third token block
     (2000, 700, 64, 1.0),    # D = 64: two steps, fewer than the ring's stages
     (1024, 3000, 192, 1.3),  # D = 192: six steps (the ring wraps once, ragged)
-    (520, 1, 64, 1.0),       # one vocabulary entry in a 256-row chunk: logp = 0
+    (520, 1, 64, 1.0),       # one vocabulary entry in a 384-row chunk: logp = 0
 ])
 def test_token_logprob_vs_oracle(device, N, V, D, scale):
     say(f"token_logprob N={N} V={V} D={D} scale={scale}")
@@ -118,8 +118,8 @@ def packed_layout(W_bits, V, D):
     """The packed LM-head layout restated from its definition: 16-byte unit
     ((tile * D/64 + s) * 4 + u) * 64 + lane holds row 32 tile + lane % 32,
     dims 64 s + 32 (lane / 32) + 8 u + 0..7; rows past V (up to a multiple of
-    256) are zeros."""
-    Vp = (V + 255) // 256 * 256
+    384) are zeros."""
+    Vp = (V + 383) // 384 * 384
     Wz = np.zeros((Vp, D), np.uint16)
     Wz[:V] = W_bits
     x = Wz.reshape(Vp // 32, 32, D // 64, 2, 4, 8)      # tile, row, s, half, u, e
@@ -134,7 +134,7 @@ def test_pack_weight_layout(device, V, D):
     _, W = inputs(V + D, 1, V, D, device)
     Wp = ra.token_logprob_pack_weight(W)
     torch.cuda.synchronize()
-    assert Wp.numel() == (V + 255) // 256 * 256 * D
+    assert Wp.numel() == (V + 383) // 384 * 384 * D
     assert np.array_equal(bits(Wp), packed_layout(bits(W), V, D))
 
 
