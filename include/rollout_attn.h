@@ -47,7 +47,7 @@
  *     eager call would. Replays of one graph must not overlap in time if
  *     they share a workspace.
  *
- * Paged KV layout (ABI versions 2 to 4). Page size P = 16 tokens, head dim D = 128.
+ * Paged KV layout (ABI versions 2 to 5). Page size P = 16 tokens, head dim D = 128.
  * Logical token j of row b lives in physical page bt[b * bt_stride + j / P]
  * at slot j % P. Within a page each KV head owns one contiguous block:
  *   K pool  [num_pages][Hkv][P][D]   element (page, g, slot, d) at
@@ -83,7 +83,7 @@
 extern "C" {
 #endif
 
-#define RA_ABI_VERSION 4
+#define RA_ABI_VERSION 5
 #define RA_PAGE_SIZE 16
 #define RA_HEAD_DIM 128
 
@@ -402,7 +402,8 @@ int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t 
  * Packed layout: bf16, 16-byte units; unit
  *   i = ((tile * (D / 64) + s) * 4 + u) * 64 + lane
  * holds W[32 * tile + lane % 32][64 * s + 32 * (lane / 32) + 8 * u + 0..7],
- * zeros for rows at or past V; tiles cover V rounded up to a multiple of 384.
+ * zeros for rows at or past V; tiles cover V rounded up to a multiple of 384
+ * (256 before ABI version 5: a copy sized by an older library can be too small).
  *
  * token_logprob_packed_weight_size: bytes of the packed copy (0 if V <= 0,
  *   D <= 0 or D is not a multiple of 64).
