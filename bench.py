@@ -647,7 +647,7 @@ def logprob_leg(ra, synth, dev, steps: int, warmup: int):
         h = synth.randn_bf16((N, D), gen, dev)
         t = torch.randint(0, V, (N,), dtype=torch.int32, device=dev, generator=gen)
         out = torch.empty(N, dtype=torch.float32, device=dev)
-        ws = torch.empty(ra.token_logprob_workspace_size(N, V), dtype=torch.uint8, device=dev)
+        ws = torch.empty(ra.token_logprob_workspace_size(N, V, D), dtype=torch.uint8, device=dev)
         nbytes = V * D * 2 + N * D * 2 + N * 8
         flops = 2 * N * V * D
         for key, fn in ((f"N{N}", lambda: ra.token_logprob(h, W, t, 1.0, out=out, workspace=ws)),

@@ -381,13 +381,15 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
  *   scale      multiplies the logits (1 / temperature; 1 for the raw model)
  *   logprob    fp32 [N]
  *   lse        fp32 [N] or NULL
- *   workspace  device scratch of at least token_logprob_workspace_size(N, V)
- *              bytes (per-chunk partials; contents on entry ignored)
+ *   workspace  device scratch of at least token_logprob_workspace_size(N, V, D)
+ *              bytes (per-chunk partials and, from N = 512 on, a copy of h in
+ *              the order the large-batch kernel loads it: N rounded up to 256
+ *              rows x D bf16; contents on entry ignored)
  * Errors: RA_ERR_NULL; RA_ERR_SHAPE (N < 0, V <= 0, D <= 0);
  *         RA_ERR_UNSUPPORTED (D not a multiple of 64); RA_ERR_WORKSPACE;
  *         RA_ERR_HIP. N == 0 returns RA_OK without launching anything.
  */
-size_t token_logprob_workspace_size(int32_t N, int32_t V);
+size_t token_logprob_workspace_size(int32_t N, int32_t V, int32_t D);
 int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t N, int32_t V,
                   int32_t D, float scale, float *logprob, float *lse, void *workspace,
                   size_t workspace_bytes, hipStream_t stream);

@@ -530,8 +530,8 @@ def kv_page_gather(kv: PagedKV, lens: torch.Tensor, cu_out: torch.Tensor,
     return k_out, v_out
 
 
-def token_logprob_workspace_size(N: int, V: int) -> int:
-    return int(_lib.load().token_logprob_workspace_size(N, V))
+def token_logprob_workspace_size(N: int, V: int, D: int) -> int:
+    return int(_lib.load().token_logprob_workspace_size(N, V, D))
 
 
 def _token_logprob(h, W, targets, scale, out, lse, want_lse, workspace, stream, packed_V):
@@ -563,7 +563,7 @@ def _token_logprob(h, W, targets, scale, out, lse, want_lse, workspace, stream, 
         _need(lse, "lse", torch.float32, dev)
         _shape(lse, (N,), "lse")
     if workspace is None:
-        workspace = _empty(max(lib.token_logprob_workspace_size(N, V), 1), torch.uint8, dev,
+        workspace = _empty(max(lib.token_logprob_workspace_size(N, V, D), 1), torch.uint8, dev,
                            stream)
     _need(workspace, "workspace", torch.uint8, dev)
     fn = lib.token_logprob if packed_V is None else lib.token_logprob_packed

@@ -111,7 +111,7 @@ def load() -> ctypes.CDLL:
                                        vp, vp, vp, kvp, i32, i32, i32, i32, vp, vp,
                                        i32, f32, vp, sz, vp]
     lib.rollout_attn_mixed.restype = ctypes.c_int
-    lib.token_logprob_workspace_size.argtypes = [i32, i32]
+    lib.token_logprob_workspace_size.argtypes = [i32, i32, i32]
     lib.token_logprob_workspace_size.restype = sz
     lib.token_logprob.argtypes = [vp, vp, vp, i32, i32, i32, f32, vp, vp, vp, sz, vp]
     lib.token_logprob.restype = ctypes.c_int

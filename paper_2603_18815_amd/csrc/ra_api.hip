@@ -378,9 +378,9 @@ int rollout_attn_mixed(const void *q_decode, const ra_paged_kv *kv_decode,
       stream));
 }
 
-size_t token_logprob_workspace_size(int32_t N, int32_t V) {
-  if (N <= 0 || V <= 0) return 0;
-  return ra::logprob_workspace_bytes(N, V);
+size_t token_logprob_workspace_size(int32_t N, int32_t V, int32_t D) {
+  if (N <= 0 || V <= 0 || D <= 0 || D % 64 != 0) return 0;
+  return ra::logprob_workspace_bytes(N, V, D);
 }
 
 int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t N, int32_t V,
@@ -391,7 +391,7 @@ int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t 
   if (D % 64 != 0) return RA_ERR_UNSUPPORTED;
   if (N == 0) return RA_OK;
   if (ra::logprob_grid(N, V) > 0x7fffffff) return RA_ERR_UNSUPPORTED;
-  if (!workspace || workspace_bytes < ra::logprob_workspace_bytes(N, V)) return RA_ERR_WORKSPACE;
+  if (!workspace || workspace_bytes < ra::logprob_workspace_bytes(N, V, D)) return RA_ERR_WORKSPACE;
   return hip_status(ra::launch_logprob(static_cast<const uint16_t *>(h),
                                        static_cast<const uint16_t *>(W), targets, N, V, D, scale,
                                        logprob, lse, workspace, false, stream));
@@ -420,7 +420,7 @@ int token_logprob_packed(const void *h, const void *W_packed, const int32_t *tar
   if (D % 64 != 0) return RA_ERR_UNSUPPORTED;
   if (N == 0) return RA_OK;
   if (ra::logprob_grid(N, V) > 0x7fffffff) return RA_ERR_UNSUPPORTED;
-  if (!workspace || workspace_bytes < ra::logprob_workspace_bytes(N, V)) return RA_ERR_WORKSPACE;
+  if (!workspace || workspace_bytes < ra::logprob_workspace_bytes(N, V, D)) return RA_ERR_WORKSPACE;
   return hip_status(ra::launch_logprob(static_cast<const uint16_t *>(h),
                                        static_cast<const uint16_t *>(W_packed), targets, N, V, D,
                                        scale, logprob, lse, workspace, true, stream));

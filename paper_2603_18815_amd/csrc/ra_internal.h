@@ -84,7 +84,7 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
 
 // ---- per-token log-probabilities under an LM head ----
 int32_t logprob_chunks(int32_t N, int32_t V);
-size_t logprob_workspace_bytes(int32_t N, int32_t V);
+size_t logprob_workspace_bytes(int32_t N, int32_t V, int32_t D);
 int64_t logprob_grid(int32_t N, int32_t V);
 hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *targets, int32_t N,
                           int32_t V, int32_t D, float scale, float *logp, float *lse,

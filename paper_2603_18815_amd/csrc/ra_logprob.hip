@@ -57,6 +57,7 @@ constexpr int kWaitVm0 = 0x0F70;
 
 struct LogprobArgs {
   const uint16_t *h;
+  const uint16_t *hp;   // N >= kTileMinN: h in the tiled kernel's LDS stage order (workspace)
   const uint16_t *W;
   const int32_t *targets;
   float *ws_m;    // [N][chunks] running max, base-2 units
@@ -326,13 +327,13 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     ga[k] = kPacked ? a.W + (((size_t)(v / 32) * (a.D / 64)) * 4 + lc) * kWave * 8 + (v % 32) * 8
                     : a.W + (size_t)min(v, a.V - 1) * a.D + 8 * lc;
   }
-#pragma unroll
-  for (int k = 0; k < kLoadsB; ++k) {
-    const int r = 16 * (kLoadsB * wave + k) + lane / 4;
-    const int lc = (lane % 4) ^ ((r >> 2) & 3);
-    gb[k] = a.h + (size_t)min(t0 + r, a.N - 1) * a.D + 8 * lc;
-  }
   const int nsteps = a.D / kTileDims;
+  // h comes from its staged copy, which holds each (token block, step) as the
+  // 16 KB image of its LDS region: load instruction j reads 1 KB contiguous
+#pragma unroll
+  for (int k = 0; k < kLoadsB; ++k)
+    gb[k] = a.hp + (size_t)tblock * nsteps * kTileElems + (size_t)(kLoadsB * wave + k) * 512 +
+            lane * 8;
   const int last = nsteps - 1;
   const uint32_t blkA = (uint32_t)(kLoadsA * wave) * 1024u, blkB = (uint32_t)(kLoadsB * wave) * 1024u;
   // offsets (elements) of step s in W and h; steps past the last repeat it
@@ -344,7 +345,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     if (d < kLoadsA)
       load_lds16(ga[d] + w_off(s), lds_address(sA[st]) + blkA + 1024u * d);
     else
-      load_lds16(gb[d - kLoadsA] + (size_t)s * kTileDims,
+      load_lds16(gb[d - kLoadsA] + (size_t)s * kTileElems,
                  lds_address(sB[st]) + blkB + 1024u * (d - kLoadsA));
   };
   constexpr int kLoadsPerStep = kLoadsA + kLoadsB;
@@ -457,6 +458,27 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
   }
 }
 
+// h staged for the tiled kernel: 16-byte unit u = ((tb * steps + s) * 256 + r) * 4
+// + slot holds token 256 tb + r (zeros past N), dims 32 s + 8 (slot ^ ((r / 4) % 4))
+// + 0..7 -- the LDS image of token block tb's step s.
+__global__ __launch_bounds__(256) void logprob_stage_h_kernel(const uint16_t *__restrict__ h,
+                                                              int32_t N, int32_t D, size_t units,
+                                                              uint16_t *__restrict__ hp) {
+  const size_t steps = (size_t)(D / kTileDims);
+  for (size_t u = (size_t)blockIdx.x * blockDim.x + threadIdx.x; u < units;
+       u += (size_t)gridDim.x * blockDim.x) {
+    const int slot = (int)(u & 3);
+    const size_t row = u >> 2;
+    const int r = (int)(row % kTileRows);
+    const size_t q = row / kTileRows, s = q % steps, tb = q / steps;
+    const size_t t = tb * kTileRows + r;
+    const int lc = slot ^ ((r >> 2) & 3);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (t < (size_t)N) v = load_u32x4(h + t * D + kTileDims * s + 8 * lc);
+    store_u32x4(hp + 8 * u, v);
+  }
+}
+
 // Packed copy of W: 16-byte unit i = ((tile * D/64 + s) * 4 + u) * 64 + lane
 // holds W[32 tile + lane % 32][64 s + 32 (lane / 32) + 8 u + 0..7] (zeros for
 // rows past V).
@@ -523,8 +545,19 @@ hipError_t launch_logprob_pack(const uint16_t *W, int32_t V, int32_t D, uint16_t
   return hipGetLastError();
 }
 
-size_t logprob_workspace_bytes(int32_t N, int32_t V) {
+namespace {
+// per-(token, chunk) partials and the target logits
+size_t logprob_partial_bytes(int32_t N, int32_t V) {
   return ((size_t)N * logprob_chunks(N, V) * 2 + (size_t)N) * sizeof(float);
+}
+}  // namespace
+
+// The partials, then (from N = kTileMinN) the staged copy of h at the next
+// 256-byte boundary: N rounded up to whole 256-token blocks x D bf16.
+size_t logprob_workspace_bytes(int32_t N, int32_t V, int32_t D) {
+  const size_t partials = (logprob_partial_bytes(N, V) + 255) / 256 * 256;
+  if (N < kTileMinN) return logprob_partial_bytes(N, V);
+  return partials + (size_t)((N + kTileRows - 1) / kTileRows) * kTileRows * D * sizeof(uint16_t);
 }
 
 namespace {
@@ -544,6 +577,7 @@ hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *t
                           void *workspace, bool packed, hipStream_t stream) {
   LogprobArgs a;
   a.h = h;
+  a.hp = nullptr;
   a.W = W;
   a.targets = targets;
   a.N = N;
@@ -558,6 +592,17 @@ hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *t
   a.scale = scale;
   a.scale_log2 = scale * kLog2e;
   const dim3 grid((unsigned)logprob_grid(N, V));
+  if (N >= kTileMinN) {
+    uint16_t *hp = reinterpret_cast<uint16_t *>(static_cast<char *>(workspace) +
+                                                (logprob_partial_bytes(N, V) + 255) / 256 * 256);
+    a.hp = hp;
+    const size_t units = (size_t)a.token_blocks * kTileRows * D / 8;
+    const size_t want = (units + 255) / 256, blocks = want < 65536 ? want : 65536;
+    hipLaunchKernelGGL(logprob_stage_h_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, h, N,
+                       D, units, hp);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (N >= kTileMinN && packed)
     hipLaunchKernelGGL(logprob_tile_kernel<true>, grid, dim3(kTileThreads), 0, stream, a);
   else if (N >= kTileMinN)

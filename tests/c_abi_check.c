@@ -92,7 +92,7 @@ int main(void) {
          rollout_attn_mixed(fake, &kv, ifake, 2, 64, ffake, NULL, NULL, ifake, ifake, &kv, 2,
                             10, 5, 64, ffake, NULL, 4, 0.1f, ws, sizeof ws, 0),
          RA_ERR_NULL);
-  expect("logprob workspace", (int)(token_logprob_workspace_size(8, 100) > 0), 1);
+  expect("logprob workspace", (int)(token_logprob_workspace_size(8, 100, 128) > 0), 1);
   expect("logprob: D not a multiple of 64",
          token_logprob(fake, fake, ifake, 8, 100, 96, 1.0f, ffake, NULL, ws, sizeof ws, 0),
          RA_ERR_UNSUPPORTED);

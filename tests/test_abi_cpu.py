@@ -129,10 +129,15 @@ def test_token_logprob_validation(lib):
     assert call(ws_bytes=4) == _lib.RA_ERR_WORKSPACE
     assert call(N=0) == _lib.RA_OK
     f = lib.token_logprob_workspace_size
-    assert f(0, 100) == 0 and f(8, 0) == 0
-    assert f(64, 151936) == (64 * 1187 * 2 + 64) * 4     # 1187 chunks of 128 rows
-    assert f(511, 151936) == (511 * 1187 * 2 + 511) * 4
-    assert f(512, 151936) == (512 * 396 * 2 + 512) * 4   # from N = 512: 396 chunks of 384 rows
+    assert f(0, 100, 128) == 0 and f(8, 0, 128) == 0
+    assert f(8, 100, 0) == 0 and f(8, 100, 96) == 0      # D not a positive multiple of 64
+    assert f(64, 151936, 4096) == (64 * 1187 * 2 + 64) * 4     # 1187 chunks of 128 rows
+    assert f(511, 151936, 4096) == (511 * 1187 * 2 + 511) * 4
+    # from N = 512: 396 chunks of 384 rows, then (at a 256-byte boundary) the
+    # staged copy of h, N rounded up to whole 256-token blocks
+    for N, padded in ((512, 512), (513, 768)):
+        part = (N * 396 * 2 + N) * 4
+        assert f(N, 151936, 4096) == (part + 255) // 256 * 256 + padded * 4096 * 2
 
 
 def test_token_logprob_packed_validation(lib):

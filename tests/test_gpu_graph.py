@@ -155,8 +155,8 @@ def test_fp8_rope_logprob_step_replays_in_a_graph(device):
     ws_d = torch.empty(ra.decode_workspace_size(Bd, w.Hq, Hkv, mk), **u8)
     ws_f = torch.empty(ra.append_workspace_size(Ba, w.Hq, Hkv, mq), **u8)
     ws_m = torch.empty(ra.mixed_workspace_size(Bd, Ba, w.Hq, Hkv, Hkv, mk, mq), **u8)
-    ws_l = torch.empty(ra.token_logprob_workspace_size(N, V), **u8)
-    ws_p = torch.empty(ra.token_logprob_workspace_size(N, V), **u8)
+    ws_l = torch.empty(ra.token_logprob_workspace_size(N, V, 128), **u8)
+    ws_p = torch.empty(ra.token_logprob_workspace_size(N, V, 128), **u8)
 
     def step():
         ra.kv_page_write(t.k_new, t.v_new, cu_w_t, st_w_t, kw, max_new, max_pos, cos_sin=tab)
@@ -205,8 +205,8 @@ def test_shared_prefix_and_large_batch_logprob_replay_in_a_graph(device):
     ws = torch.empty(ra.decode_shared_prefix_workspace_size(B, Hq, Hkv, mk, mp), **u8)
     lp, lp_lse = torch.empty((N,), **f32), torch.empty((N,), **f32)
     lpp, lpp_lse = torch.empty((N,), **f32), torch.empty((N,), **f32)
-    ws_l = torch.empty(ra.token_logprob_workspace_size(N, V), **u8)
-    ws_p = torch.empty(ra.token_logprob_workspace_size(N, V), **u8)
+    ws_l = torch.empty(ra.token_logprob_workspace_size(N, V, D), **u8)
+    ws_p = torch.empty(ra.token_logprob_workspace_size(N, V, D), **u8)
 
     def step():
         ra.decode_shared_prefix(q, kv, lens_t, gs_t, pre_t, mg, mp, mk, SCALE, out=out, lse=lse,
