@@ -26,7 +26,7 @@
 // From N = 512 on, the partials come from the 384 x 256 tiled kernel further
 // down (384-row chunks) instead.
 //
-// Combine kernel: one wave per token merges its partials in chunk order:
+// Combine kernel: one workgroup per token merges its partials:
 // M = max_c m_c, L = sum_c l_c 2^(m_c - M), lse = (M + log2 L) ln 2.
 //
 // Packed LM head: W [V][D] row-major makes every wave read 32 rows 128 bytes
@@ -500,22 +500,29 @@ __global__ __launch_bounds__(256) void logprob_pack_kernel(const uint16_t *__res
 
 __global__ __launch_bounds__(kLpThreads) void logprob_combine_kernel(LogprobArgs a, float *logp,
                                                                    float *lse) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int t = blockIdx.x * kLpWaves + threadIdx.x / kWave;
-  if (t >= a.N) return;
+  // One workgroup per token: thread i folds chunks i, i + 256, ... in order;
+  // the lanes of a wave are combined by a fixed butterfly and the four waves
+  // in wave order, so the result does not depend on timing.
+  __shared__ float s_red[2][kLpWaves];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int t = blockIdx.x;
   const float *m = a.ws_m + (size_t)t * a.chunks;
   const float *l = a.ws_l + (size_t)t * a.chunks;
-  // Each lane folds chunks lane, lane + 64, ... in order; the lanes are then
-  // combined by a fixed butterfly, so the result does not depend on timing.
   float M = -INFINITY;
-  for (int c = lane; c < a.chunks; c += kWave) M = fmaxf(M, m[c]);
+  for (int c = threadIdx.x; c < a.chunks; c += kLpThreads) M = fmaxf(M, m[c]);
 #pragma unroll
   for (int o = 1; o < kWave; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
+  if (lane == 0) s_red[0][wave] = M;
+  __syncthreads();
+  M = fmaxf(fmaxf(s_red[0][0], s_red[0][1]), fmaxf(s_red[0][2], s_red[0][3]));
   float L = 0.f;
-  for (int c = lane; c < a.chunks; c += kWave) L += l[c] * fast_exp2(m[c] - M);
+  for (int c = threadIdx.x; c < a.chunks; c += kLpThreads) L += l[c] * fast_exp2(m[c] - M);
 #pragma unroll
   for (int o = 1; o < kWave; o <<= 1) L += __shfl_xor(L, o);
-  if (lane == 0) {
+  if (lane == 0) s_red[1][wave] = L;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    L = ((s_red[1][0] + s_red[1][1]) + s_red[1][2]) + s_red[1][3];
     const float ls = (M + __log2f(L)) * kLn2;
     const int target = a.targets[t];
     logp[t] = target >= 0 && target < a.V ? a.tgt[t] - ls : __builtin_nanf("");
@@ -619,8 +626,8 @@ hipError_t launch_logprob(const uint16_t *h, const uint16_t *W, const int32_t *t
                        stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(logprob_combine_kernel, dim3((N + kLpWaves - 1) / kLpWaves),
-                     dim3(kLpThreads), 0, stream, a, logp, lse);
+  hipLaunchKernelGGL(logprob_combine_kernel, dim3((unsigned)N), dim3(kLpThreads), 0, stream, a,
+                     logp, lse);
   return hipGetLastError();
 }
 
