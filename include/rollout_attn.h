@@ -47,7 +47,7 @@
  *     eager call would. Replays of one graph must not overlap in time if
  *     they share a workspace.
  *
- * Paged KV layout (ABI versions 2 to 5). Page size P = 16 tokens, head dim D = 128.
+ * Paged KV layout (ABI versions 2 to 6). Page size P = 16 tokens, head dim D = 128.
  * Logical token j of row b lives in physical page bt[b * bt_stride + j / P]
  * at slot j % P. Within a page each KV head owns one contiguous block:
  *   K pool  [num_pages][Hkv][P][D]   element (page, g, slot, d) at
@@ -83,7 +83,7 @@
 extern "C" {
 #endif
 
-#define RA_ABI_VERSION 5
+#define RA_ABI_VERSION 6
 #define RA_PAGE_SIZE 16
 #define RA_HEAD_DIM 128
 
@@ -397,15 +397,18 @@ int token_logprob(const void *h, const void *W, const int32_t *targets, int32_t 
 /*
  * The same log-probabilities from a packed copy of the LM-head matrix. The
  * matrix is constant for a policy version, so it can be repacked once into
- * the order the kernel's matrix products consume it; each wave then streams
- * one contiguous run of memory instead of 32 rows 128 bytes at a time.
+ * the order the kernel's matrix products consume it; each wave then reads
+ * 4 KB contiguous per 64-dim step instead of 32 rows 128 bytes at a time,
+ * and the waves on one step read one narrow window of memory.
  * Results are bitwise those of token_logprob on the unpacked matrix.
  *
- * Packed layout: bf16, 16-byte units; unit
- *   i = ((tile * (D / 64) + s) * 4 + u) * 64 + lane
+ * Packed layout: bf16, 16-byte units; with T = ceil(V / 384) * 12 tiles of
+ * 32 rows (V rounded up to a multiple of 384), unit
+ *   i = ((s * T + tile) * 4 + u) * 64 + lane
  * holds W[32 * tile + lane % 32][64 * s + 32 * (lane / 32) + 8 * u + 0..7],
- * zeros for rows at or past V; tiles cover V rounded up to a multiple of 384
- * (256 before ABI version 5: a copy sized by an older library can be too small).
+ * zeros for rows at or past V. ABI versions 4 and 5 stored the units tile by
+ * tile, i = ((tile * (D / 64) + s) * 4 + u) * 64 + lane, and version 4 rounded
+ * V up to 256 rows: a copy made by an older library must be packed again.
  *
  * token_logprob_packed_weight_size: bytes of the packed copy (0 if V <= 0,
  *   D <= 0 or D is not a multiple of 64).

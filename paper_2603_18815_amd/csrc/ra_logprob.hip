@@ -30,11 +30,13 @@
 // M = max_c m_c, L = sum_c l_c 2^(m_c - M), lse = (M + log2 L) ln 2.
 //
 // Packed LM head: W [V][D] row-major makes every wave read 32 rows 128 bytes
-// at a time, 8 KB apart. The packed copy stores each 32-row tile in the order
-// the products consume it, [V/32][D/64][4][64 lanes][8], so a wave's whole
-// stream over D is one contiguous run and each load instruction reads 1 KB
-// contiguous. Same products in the same order: the results are bitwise those
-// of the row-major matrix.
+// at a time, 8 KB apart. The packed copy stores the matrix in the order the
+// products consume it, [D/64][tiles][4][64 lanes][8] (32-row tiles, V rounded
+// up to whole 384-row chunks): each load instruction reads 1 KB contiguous,
+// a wave's step is 4 KB contiguous, and the waves working on one 64-dim step
+// at the same time read one narrow window of memory rather than thousands of
+// separate runs. Same products in the same order: the results are bitwise
+// those of the row-major matrix.
 #include "ra_device.h"
 #include "ra_internal.h"
 
@@ -107,7 +109,7 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   // (packed: rows past V are stored as zeros); rows past V are masked after
   // the products.
   const uint16_t *wp =
-      kPacked ? a.W + (size_t)(v0 / 32) * 32 * a.D + 8 * lane
+      kPacked ? a.W + (size_t)(v0 / 32) * 4 * kWave * 8 + 8 * lane
               : a.W + (size_t)min(v0 + col, a.V - 1) * a.D + 32 * half;
   // h staging: thread i copies 16-byte chunks i + 256 j (j = 0..3) of the
   // block's 128 x 64 slice (token = chunk / 8, 8 dims per chunk); tokens past
@@ -139,12 +141,14 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   // those loads are marked nontemporal. Row-major loads take each line 32
   // bytes at a time over four instructions and stay ordinary.
   constexpr bool kStreamW = kPacked && kTiles == 2;
+  // 32-row tiles of the packed copy: a 64-dim step of all of them is one block
+  const size_t ntiles = (size_t)((a.V + kPackRows - 1) / kPackRows) * (kPackRows / 32);
   bf16x8 w0[4], w1[4], w2[4], w3[4];
   auto w_load = [&](bf16x8 *dst, int s) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      dst[u] = kStreamW ? __builtin_bit_cast(bf16x8, load_stream_u32x4(wp + (size_t)(4 * s + u) * 8 * kWave))
-                        : load_bf16x8(kPacked ? wp + (size_t)(4 * s + u) * 8 * kWave
+      dst[u] = kStreamW ? __builtin_bit_cast(bf16x8, load_stream_u32x4(wp + ((size_t)s * ntiles * 4 + u) * 8 * kWave))
+                        : load_bf16x8(kPacked ? wp + ((size_t)s * ntiles * 4 + u) * 8 * kWave
                                               : wp + s * kDimStep + 8 * u);
   };
   const int nsteps = a.D / kDimStep;
@@ -322,9 +326,9 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     const int r = 16 * (kLoadsA * wave + k) + lane / 4;
     const int lc = (lane % 4) ^ ((r >> 2) & 3);
     const int v = v0 + r;
-    // packed: 16-byte unit ((tile * D/64 + s / 2) * 4 + lc) * 64 + 32 (s % 2) + v % 32
+    // packed: 16-byte unit ((s / 2 * tiles + tile) * 4 + lc) * 64 + 32 (s % 2) + v % 32
     // (the part that depends on the step s is added per step)
-    ga[k] = kPacked ? a.W + (((size_t)(v / 32) * (a.D / 64)) * 4 + lc) * kWave * 8 + (v % 32) * 8
+    ga[k] = kPacked ? a.W + ((size_t)(v / 32) * 4 + lc) * kWave * 8 + (v % 32) * 8
                     : a.W + (size_t)min(v, a.V - 1) * a.D + 8 * lc;
   }
   const int nsteps = a.D / kTileDims;
@@ -338,8 +342,10 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
   const uint32_t blkA = (uint32_t)(kLoadsA * wave) * 1024u, blkB = (uint32_t)(kLoadsB * wave) * 1024u;
   // offsets (elements) of step s in W and h; steps past the last repeat it
   // (branch-free, so that every step issues the same number of loads)
+  // elements per 64-dim step of the packed copy (all of its 32-row tiles)
+  const size_t pstride = (size_t)((a.V + kPackRows - 1) / kPackRows) * (kPackRows / 32) * 4 * kWave * 8;
   auto w_off = [&](int s) __attribute__((always_inline)) {
-    return kPacked ? (size_t)(s >> 1) * 4 * kWave * 8 + (s & 1) * 32 * 8 : (size_t)s * kTileDims;
+    return kPacked ? (size_t)(s >> 1) * pstride + (s & 1) * 32 * 8 : (size_t)s * kTileDims;
   };
   auto load = [&](int st, int s, int d) __attribute__((always_inline)) {
     if (d < kLoadsA)
@@ -479,9 +485,9 @@ __global__ __launch_bounds__(256) void logprob_stage_h_kernel(const uint16_t *__
   }
 }
 
-// Packed copy of W: 16-byte unit i = ((tile * D/64 + s) * 4 + u) * 64 + lane
+// Packed copy of W: 16-byte unit i = ((s * tiles + tile) * 4 + u) * 64 + lane
 // holds W[32 tile + lane % 32][64 s + 32 (lane / 32) + 8 u + 0..7] (zeros for
-// rows past V).
+// rows past V; tiles = the copy's rows / 32).
 __global__ __launch_bounds__(256) void logprob_pack_kernel(const uint16_t *__restrict__ W,
                                                            int32_t V, int32_t D, size_t units,
                                                            uint16_t *__restrict__ Wp) {
@@ -489,7 +495,8 @@ __global__ __launch_bounds__(256) void logprob_pack_kernel(const uint16_t *__res
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < units;
        i += (size_t)gridDim.x * blockDim.x) {
     const int lane = (int)(i % kWave), u = (int)((i / kWave) % 4);
-    const size_t s = (i / (4 * kWave)) % steps, tile = i / (4 * kWave * steps);
+    const size_t ntiles = units / (4 * kWave * steps);
+    const size_t tile = (i / (4 * kWave)) % ntiles, s = i / (4 * kWave * ntiles);
     const size_t row = 32 * tile + (lane & 31);
     const size_t dim = kDimStep * s + 32 * (lane >> 5) + 8 * u;
     u32x4 v = {0u, 0u, 0u, 0u};

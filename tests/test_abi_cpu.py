@@ -42,7 +42,7 @@ def test_exports_every_declared_symbol(lib):
 
 def test_abi_version_and_status_strings(lib):
     declared = int(re.search(r"#define RA_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
-    assert lib.ra_abi_version() == declared == 5
+    assert lib.ra_abi_version() == declared == 6
     assert lib.ra_status_string(0) == b"RA_OK"
     assert lib.ra_status_string(4) == b"RA_ERR_WORKSPACE"
     assert lib.ra_status_string(99) == b"RA_UNKNOWN_STATUS"

@@ -115,15 +115,15 @@ def test_token_logprob_qwen3_lm_head(device):
 
 
 def packed_layout(W_bits, V, D):
-    """The packed LM-head layout restated from its definition: 16-byte unit
-    ((tile * D/64 + s) * 4 + u) * 64 + lane holds row 32 tile + lane % 32,
-    dims 64 s + 32 (lane / 32) + 8 u + 0..7; rows past V (up to a multiple of
-    384) are zeros."""
+    """The packed LM-head layout restated from its definition: with T tiles of
+    32 rows (V rounded up to a multiple of 384), 16-byte unit
+    ((s * T + tile) * 4 + u) * 64 + lane holds row 32 tile + lane % 32, dims
+    64 s + 32 (lane / 32) + 8 u + 0..7; rows past V are zeros."""
     Vp = (V + 383) // 384 * 384
     Wz = np.zeros((Vp, D), np.uint16)
     Wz[:V] = W_bits
     x = Wz.reshape(Vp // 32, 32, D // 64, 2, 4, 8)      # tile, row, s, half, u, e
-    x = x.transpose(0, 2, 4, 3, 1, 5)                   # tile, s, u, half, row, e
+    x = x.transpose(2, 0, 4, 3, 1, 5)                   # s, tile, u, half, row, e
     return x.reshape(-1)                                # lane = 32 half + row
 
 
