@@ -404,6 +404,14 @@ def test_logprob_closed_forms():
     logp, lse = oracle.token_logprob(h, W, [-1, V, 3])
     assert np.isnan(logp[0]) and np.isnan(logp[1]) and np.isfinite(logp[2])
     assert np.all(np.isfinite(lse))
+    # logits of 1000 and 996 (exact in bf16): exp overflows fp64 unless the
+    # maximum is taken out first; lse = 1000 + ln(1 + e^-4)
+    h = bf16_bits([[1.0, 0.0]] * 2)
+    W = bf16_bits([[1000.0, 0.0], [996.0, 0.0]])
+    logp, lse = oracle.token_logprob(h, W, [0, 1])
+    np.testing.assert_allclose(lse, 1000.0 + math.log1p(math.exp(-4.0)), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(logp, [-math.log1p(math.exp(-4.0)), -4.0 - math.log1p(math.exp(-4.0))],
+                               rtol=0, atol=1e-12)
 
 
 def test_logprob_normalised_and_shift_invariant():
