@@ -89,6 +89,42 @@ def test_token_logprob_peaked_and_flat(device):
     np.testing.assert_allclose(lp[:8].cpu().numpy(), -math.log(V), atol=1e-5, rtol=0)
 
 
+@pytest.mark.parametrize("N", [4, 520])
+def test_token_logprob_logits_near_1000(device, N):
+    """Logits up to ~1,016, far past where exp overflows fp32 unless the
+    maximum is taken out first: W[v] = (1000 - 4 (v % 97), small integer) and
+    h[n] = (1, n % 5 - 2), all exact in bf16, so every logit is an exact
+    integer in fp32 too. N = 4 runs the partial kernel, N = 520 the tiled one,
+    both layouts of W. The remaining error is fp32 rounding of values near
+    1,000 (and near 1,443 in base-2 units): a few 1e-4, so this test allows
+    5e-4 absolute."""
+    say(f"token_logprob logits near 1000 N={N}")
+    V, D = 700, 64
+    v = np.arange(V)
+    Wf = np.zeros((V, D), np.float32)
+    Wf[:, 0] = 1000 - 4 * (v % 97)
+    Wf[:, 1] = (v * 7) % 17 - 8
+    hf = np.zeros((N, D), np.float32)
+    hf[:, 0] = 1.0
+    hf[:, 1] = np.arange(N) % 5 - 2
+    W = torch.from_numpy(Wf).to(torch.bfloat16).to(device)
+    h = torch.from_numpy(hf).to(torch.bfloat16).to(device)
+    assert torch.equal(W.float().cpu(), torch.from_numpy(Wf)) and torch.equal(h.float().cpu(), torch.from_numpy(hf))
+    t = torch.from_numpy((np.arange(N) * 37 % V).astype(np.int32)).to(device)
+    lp, ls = ra.token_logprob(h, W, t, 1.0, want_lse=True)
+    lq, lsq = ra.token_logprob_packed(h, ra.token_logprob_pack_weight(W), V, t, 1.0, want_lse=True)
+    torch.cuda.synchronize()
+    ref_lp, ref_ls = oracle.token_logprob(bits(h), bits(W), t.cpu().numpy(), 1.0)
+    assert np.all(ref_ls > 999.0)
+    for a, b, what in ((lp, ls, "row-major"), (lq, lsq, "packed")):
+        a, b = a.cpu().numpy().astype(np.float64), b.cpu().numpy().astype(np.float64)
+        assert np.all(np.isfinite(a)) and np.all(np.isfinite(b)), what
+        err_lp, err_ls = float(np.abs(a - ref_lp).max()), float(np.abs(b - ref_ls).max())
+        print(f"[parity] logits near 1000 N={N} {what}: max|dlogp|={err_lp:.2e} max|dlse|={err_ls:.2e}", flush=True)
+        assert err_lp <= 5e-4 and err_ls <= 5e-4, (what, err_lp, err_ls)
+    assert torch.equal(lp, lq) and torch.equal(ls, lsq)
+
+
 def test_token_logprob_deterministic(device):
     N, V, D = 64, 5000, 256
     h, W = inputs(9, N, V, D, device)
