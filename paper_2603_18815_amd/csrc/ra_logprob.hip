@@ -142,7 +142,7 @@ __global__ __launch_bounds__(kLpThreads, 2) void logprob_partial_kernel(LogprobA
   // bytes at a time over four instructions and stay ordinary.
   constexpr bool kStreamW = kPacked && kTiles == 2;
   // 32-row tiles of the packed copy: a 64-dim step of all of them is one block
-  const size_t ntiles = (size_t)((a.V + kPackRows - 1) / kPackRows) * (kPackRows / 32);
+  const size_t ntiles = (size_t)(((int64_t)a.V + kPackRows - 1) / kPackRows) * (kPackRows / 32);
   bf16x8 w0[4], w1[4], w2[4], w3[4];
   auto w_load = [&](bf16x8 *dst, int s) __attribute__((always_inline)) {
 #pragma unroll
@@ -343,7 +343,8 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
   // offsets (elements) of step s in W and h; steps past the last repeat it
   // (branch-free, so that every step issues the same number of loads)
   // elements per 64-dim step of the packed copy (all of its 32-row tiles)
-  const size_t pstride = (size_t)((a.V + kPackRows - 1) / kPackRows) * (kPackRows / 32) * 4 * kWave * 8;
+  const size_t pstride =
+      (size_t)(((int64_t)a.V + kPackRows - 1) / kPackRows) * (kPackRows / 32) * 4 * kWave * 8;
   auto w_off = [&](int s) __attribute__((always_inline)) {
     return kPacked ? (size_t)(s >> 1) * pstride + (s & 1) * 32 * 8 : (size_t)s * kTileDims;
   };
@@ -541,13 +542,13 @@ __global__ __launch_bounds__(kLpThreads) void logprob_combine_kernel(LogprobArgs
 
 int32_t logprob_chunks(int32_t N, int32_t V) {
   const int rows = N >= kTileMinN ? kTileRowsA : kVocabChunk;
-  return (V + rows - 1) / rows;
+  return (int32_t)(((int64_t)V + rows - 1) / rows);
 }
 
 // The packed copy covers every row a workgroup reads: V rounded up to whole
 // 384-row chunks (so to whole 128-row chunks too).
 size_t logprob_packed_bytes(int32_t V, int32_t D) {
-  return (size_t)((V + kPackRows - 1) / kPackRows) * kPackRows * D * sizeof(uint16_t);
+  return (size_t)(((int64_t)V + kPackRows - 1) / kPackRows) * kPackRows * D * sizeof(uint16_t);
 }
 
 hipError_t launch_logprob_pack(const uint16_t *W, int32_t V, int32_t D, uint16_t *Wp,

@@ -145,6 +145,12 @@ def test_token_logprob_packed_validation(lib):
     assert size(151936, 4096) == 396 * 384 * 4096 * 2    # V rounded up to 384 rows
     assert size(1, 64) == 384 * 64 * 2
     assert size(0, 64) == 0 and size(10, 0) == 0 and size(10, 96) == 0
+    # the largest V: the rounding to whole 384-row chunks must not overflow
+    big = 2**31 - 1
+    assert size(big, 64) == (big + 383) // 384 * 384 * 64 * 2
+    assert lib.token_logprob_workspace_size(1, big, 64) == ((big + 127) // 128 * 2 + 1) * 4
+    assert lib.token_logprob_workspace_size(512, big, 64) == \
+        ((512 * ((big + 383) // 384) * 2 + 512) * 4 + 255) // 256 * 256 + 512 * 64 * 2
 
     def pack(**kw):
         d = dict(W=FAKE, V=100, D=128, Wp=FAKE, nbytes=1 << 30)
