@@ -98,7 +98,7 @@ hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const
                              int32_t total_new, int32_t max_new, int32_t max_pos,
                              hipStream_t stream, const float *cos_sin, int32_t rope_rows) {
   // A run of n tokens touches at most (n - 1) / 16 + 2 pages.
-  const dim3 grid((max_new + kPage - 1) / kPage + 1, kv.hkv, B);
+  const dim3 grid((unsigned)(((int64_t)max_new + kPage - 1) / kPage + 1), kv.hkv, B);
   const pwrite::WriteArgs a = pwrite::write_args(k_new, v_new, cu_new, start_pos, kv, total_new,
                                                  max_new, max_pos, cos_sin, rope_rows);
   const dim3 block(pwrite::kItemThreads);
@@ -116,7 +116,7 @@ hipError_t launch_page_write(const uint16_t *k_new, const uint16_t *v_new, const
 hipError_t launch_page_gather(const PagedKV &kv, const int32_t *lens, const int32_t *cu_out,
                               int32_t B, int32_t total, int32_t max_len, uint16_t *k_out,
                               uint16_t *v_out, hipStream_t stream) {
-  const dim3 grid((max_len + kPage - 1) / kPage, kv.hkv, B);
+  const dim3 grid((unsigned)(((int64_t)max_len + kPage - 1) / kPage), kv.hkv, B);
   if (kv.fp8)
     hipLaunchKernelGGL(page_gather_fp8_kernel, grid, dim3(kThreads), 0, stream,
                        reinterpret_cast<const uint8_t *>(kv.k_pool),

@@ -301,7 +301,7 @@ MixedLayout mixed_layout(int32_t B_decode, int32_t B_append, int32_t hq, int32_t
   MixedLayout l;
   l.plan = decode_plan(B_decode > 0 ? B_decode : 1, hkv_decode, max_kv_len_decode);
   const int32_t qpb = atile::kRowsPerGroup / (hq / hkv_append);
-  l.qblocks = max_q_len > 0 ? (max_q_len + qpb - 1) / qpb : 0;
+  l.qblocks = max_q_len > 0 ? (int32_t)(((int64_t)max_q_len + qpb - 1) / qpb) : 0;
   l.max_tiles = (int64_t)B_append * l.qblocks * hkv_append;
   l.max_splits = (int64_t)B_decode * l.plan.max_splits * hkv_decode;
   l.tiles_offset = kAlign + align_up((size_t)(B_append > 0 ? B_append : 0) * sizeof(int32_t));
@@ -342,7 +342,7 @@ hipError_t launch_mixed(const uint16_t *q_decode, const PagedKV &kv_decode,
   // the fused page write (append rows only): the chunks' tokens at ctx_lens
   const pwrite::WriteArgs w = pwrite::write_args(k_new, v_new, cu_q, ctx_lens, kv_append, total_q,
                                                  max_q_len, max_kv_len_append, cos_sin, rope_rows);
-  const int32_t write_chunks = k_new ? (max_q_len + kPage - 1) / kPage + 1 : 0;
+  const int32_t write_chunks = k_new ? (int32_t)(((int64_t)max_q_len + kPage - 1) / kPage + 1) : 0;
   const int64_t write_blocks =
       ((int64_t)B_append * kv_append.hkv * write_chunks + 3) / (kPlanThreads / pwrite::kItemThreads);
   hipLaunchKernelGGL(mixed_plan_kernel, dim3((unsigned)(1 + write_blocks)), dim3(kPlanThreads), 0,

@@ -206,6 +206,9 @@ def test_append_workspace_size(lib):
     assert a >= 32 * (2048 // 64) * 8 * 8                         # one 8-byte entry per tile
     assert f(32, 32, 8, 4096) > a
     assert f(32, 32, 8, 2048) == lib.rollout_attn_mixed_workspace_size(0, 32, 32, 8, 8, 0, 2048)
+    # the largest chunk length: query blocks are counted without overflow
+    big = f(1, 32, 8, 2**31 - 1)
+    assert big >= ((2**31 - 1 + 63) // 64) * 8 * 8 and big > f(1, 32, 8, 2**30)
 
 
 def test_page_write_and_gather_validation(lib):
