@@ -205,10 +205,12 @@ def test_token_logprob_packed_matches(device, N, V, D, scale):
     check(lp2, ls2, ref_lp, ref_ls, f"packed N={N} V={V} D={D}")
 
 
-@pytest.mark.parametrize("N", [64, 1024])
+@pytest.mark.parametrize("N", [64, 1024, 4000])
 def test_token_logprob_packed_qwen3_lm_head(device, N):
-    """The Qwen3-8B LM head at the benchmark's batch sizes: packed and row-major
-    bitwise equal; 16 sampled tokens against the oracle."""
+    """The Qwen3-8B LM head at the benchmark's batch sizes and at 4,000 tokens
+    (16 token blocks, the last one ragged; ~25 rounds of tiles): packed and
+    row-major bitwise equal; 16 sampled tokens plus the first and the last
+    against the oracle."""
     V, D = 151936, 4096
     say(f"token_logprob_packed Qwen3-8B LM head N={N}")
     h, W = inputs(80 + N, N, V, D, device)
@@ -220,6 +222,6 @@ def test_token_logprob_packed_qwen3_lm_head(device, N):
     torch.cuda.synchronize()
     assert torch.equal(lp, lp2) and torch.equal(ls, ls2)
     del Wp
-    pick = np.random.default_rng(N).choice(N, size=16, replace=False)
+    pick = np.array(sorted(set(np.random.default_rng(N).choice(N, size=16, replace=False)) | {0, N - 1}))
     ref_lp, ref_ls = oracle.token_logprob(bits(h)[pick], bits(W), t.cpu().numpy()[pick], 1.0)
-    check(lp2[pick], ls2[pick], ref_lp, ref_ls, f"packed Qwen3-8B LM head, N={N} (16 sampled)")
+    check(lp2[pick], ls2[pick], ref_lp, ref_ls, f"packed Qwen3-8B LM head, N={N} ({pick.size} sampled)")
