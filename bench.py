@@ -266,8 +266,9 @@ def long_decode_leg(ra, synth, dev, steps: int, warmup: int):
 def achievable_leg(dev):
     """What this GPU delivers to the kernels, measured now by libra_microbench.so:
     the bf16 matrix-core rate of the append kernel's product on random and on zero
-    operands with the shader clock it ran at, LDS read bandwidth, and HBM read
-    rates (streaming, and shuffled 4 KiB pages as a paged cache is read). Context
+    operands with the shader clock it ran at, LDS read bandwidth, HBM read rates
+    (streaming, and shuffled 4 KiB pages as a paged cache is read) and the rate at
+    which the L2 feeds the compute units (into LDS and into registers). Context
     for the roofline fractions, which use the published peaks."""
     import torch
 
@@ -298,6 +299,12 @@ def achievable_leg(dev):
         for kb in (1024, 2048, 4096)}
     del src
     torch.cuda.empty_cache()
+    # the L2 feeding the compute units (a 2 MiB buffer that stays in every XCD's
+    # L2), by direct global-to-LDS loads as the tiled log-prob kernel stages its
+    # operands, and by loads into registers; one and two workgroups per CU
+    res["l2_read_GB_s"] = {
+        name: round(max(mb.l2_read(lds, k * cus, 2000) for k in (1, 2)), 1)
+        for name, lds in (("to_lds", True), ("to_registers", False))}
     return res
 
 

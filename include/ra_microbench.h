@@ -69,6 +69,19 @@ int ra_mb_stream_read(const void *src, int64_t bytes, const int32_t *order, int3
 int ra_mb_block_read(const void *src, int64_t bytes, int32_t block_bytes, int32_t blocks,
                      uint32_t *sink, hipStream_t stream);
 
+/* Reads an L2-resident buffer (bytes: a power of two from 64 KiB to 16 MiB,
+ * small enough to stay in each XCD's 4 MiB L2 when at most 2 MiB) over and
+ * over: each of blocks workgroups of 256 threads runs `iters` rounds in which
+ * every wave issues 16 load instructions of 1 KiB (16 bytes per lane),
+ * walking the buffer from a per-workgroup offset. to_lds != 0: direct
+ * global-to-LDS loads (global_load_lds_dwordx4, 64 KiB of LDS per
+ * workgroup); otherwise loads into registers. Bytes moved = blocks * iters *
+ * 64 KiB (the register form reads 8 KiB more per wave). The rate at which the
+ * L2 feeds the compute units. sink: uint32 [blocks * 256]. Returns 1 for a
+ * null pointer, 2 for a bad size (or iters outside [1, 2^24]). */
+int ra_mb_l2_read(const void *src, int64_t bytes, int32_t to_lds, int32_t blocks, int32_t iters,
+                  uint32_t *sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

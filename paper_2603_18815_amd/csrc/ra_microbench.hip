@@ -182,6 +182,75 @@ __global__ __launch_bounds__(kStreamThreads) void block_read_kernel(const u32x4 
   sink[(size_t)blockIdx.x * kStreamThreads + tid] = acc[0][0] ^ acc[0][1] ^ acc[0][2] ^ acc[0][3];
 }
 
+// ---- reads that hit in the L2: direct global-to-LDS loads against loads into
+// registers. Each wave moves 16 KB per round as 16 load instructions of 1 KB
+// (16 bytes per lane) from a buffer small enough to stay in every XCD's L2.
+constexpr int kL2Loads = 16;
+constexpr int kL2Threads = 256;
+
+__device__ __forceinline__ void mb_load_lds16(const u32x4 *g, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(g)
+      : "memory");
+}
+
+// kLds: each wave's 16 loads of a round land in its own 16 KB of LDS (the
+// next round overwrites them; nothing reads LDS); the wave waits until at
+// most 8 loads are outstanding after each round. Otherwise the loads go to
+// registers in two halves of 8, the second half of a round and the first of
+// the next in flight while the other is folded into an accumulator.
+template <bool kLds>
+__global__ __launch_bounds__(kL2Threads) void l2_read_kernel(const u32x4 *src, int32_t nchunks,
+                                                             int32_t iters, uint32_t *sink) {
+  __shared__ __attribute__((aligned(1024))) u32x4 ring[kLds ? 4 * kL2Loads * 64 : 1];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+  // chunk (1 KB) of load k of round i: (first + 64 i + 16 wave + k) mod nchunks,
+  // nchunks a power of two
+  const int first = (int)((blockIdx.x * 64u) & (uint32_t)(nchunks - 1));
+  auto chunk = [&](int i, int k) __attribute__((always_inline)) {
+    return src + (size_t)((first + 64 * i + 16 * wave + k) & (nchunks - 1)) * 64 + lane;
+  };
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  if constexpr (kLds) {
+    const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)ring +
+                          (uint32_t)wave * kL2Loads * 1024u;
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+      for (int k = 0; k < kL2Loads; ++k) mb_load_lds16(chunk(i, k), base + 1024u * k);
+      __builtin_amdgcn_s_waitcnt(0x0F78);   // vmcnt(8)
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);     // vmcnt(0): every load has landed
+    __syncthreads();
+    acc = ring[threadIdx.x];
+  } else {
+    constexpr int kHalf = kL2Loads / 2;
+    u32x4 a[kHalf], b[kHalf];
+#pragma unroll
+    for (int k = 0; k < kHalf; ++k) a[k] = chunk(0, k)[0];
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+      for (int k = 0; k < kHalf; ++k) b[k] = chunk(i, kHalf + k)[0];
+#pragma unroll
+      for (int k = 0; k < kHalf; ++k) acc ^= a[k];
+#pragma unroll
+      for (int k = 0; k < kHalf; ++k) a[k] = chunk(i + 1, k)[0];
+#pragma unroll
+      for (int k = 0; k < kHalf; ++k) acc ^= b[k];
+    }
+#pragma unroll
+    for (int k = 0; k < kHalf; ++k) acc ^= a[k];
+  }
+  sink[(size_t)blockIdx.x * kL2Threads + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+}
+
 int launched() { return hipGetLastError() == hipSuccess ? 0 : 5; }
 
 }  // namespace
@@ -238,6 +307,22 @@ int ra_mb_block_read(const void *src, int64_t bytes, int32_t block_bytes, int32_
   else
     hipLaunchKernelGGL(block_read_kernel<4096>, dim3(blocks), dim3(kStreamThreads), 0, stream, s,
                        nblk, bits, sink);
+  return launched();
+}
+
+int ra_mb_l2_read(const void *src, int64_t bytes, int32_t to_lds, int32_t blocks, int32_t iters,
+                  uint32_t *sink, hipStream_t stream) {
+  if (!src || !sink) return 1;
+  if (bytes < 64 * 1024 || bytes > (int64_t)1 << 24 || (bytes & (bytes - 1)) != 0) return 2;
+  if (blocks <= 0 || iters <= 0 || iters > (1 << 24)) return 2;
+  const u32x4 *s = static_cast<const u32x4 *>(src);
+  const int32_t nchunks = (int32_t)(bytes / 1024);
+  if (to_lds)
+    hipLaunchKernelGGL(l2_read_kernel<true>, dim3(blocks), dim3(kL2Threads), 0, stream, s, nchunks,
+                       iters, sink);
+  else
+    hipLaunchKernelGGL(l2_read_kernel<false>, dim3(blocks), dim3(kL2Threads), 0, stream, s,
+                       nchunks, iters, sink);
   return launched();
 }
 

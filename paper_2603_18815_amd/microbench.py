@@ -10,7 +10,8 @@ import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libra_microbench.so")
-EXPORTS = ("ra_mb_mfma_bf16", "ra_mb_lds_read", "ra_mb_stream_read", "ra_mb_block_read")
+EXPORTS = ("ra_mb_mfma_bf16", "ra_mb_lds_read", "ra_mb_stream_read", "ra_mb_block_read",
+           "ra_mb_l2_read")
 MFMA_THREADS = 256
 MFMA_OPERANDS = MFMA_THREADS * 64
 LDS_THREADS = 512
@@ -28,6 +29,7 @@ def load() -> ctypes.CDLL:
         lib.ra_mb_lds_read.argtypes = [i32, i32, vp, vp, vp]
         lib.ra_mb_stream_read.argtypes = [vp, i64, vp, i32, vp, vp]
         lib.ra_mb_block_read.argtypes = [vp, i64, i32, i32, vp, vp]
+        lib.ra_mb_l2_read.argtypes = [vp, i64, i32, i32, i32, vp, vp]
         for f in EXPORTS:
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
@@ -146,3 +148,26 @@ def block_read(src: torch.Tensor, block_bytes: int, blocks: int, reps: int = 5):
         torch.cuda.synchronize()
         ms.append(e0.elapsed_time(e1))
     return src.numel() / (min(ms) * 1e-3) / 1e9
+
+
+def l2_read(to_lds: bool, blocks: int, iters: int, nbytes: int = 1 << 21, reps: int = 3):
+    """Rate (GB/s, best of reps) at which the L2 feeds the compute units: an
+    nbytes buffer (it stays in each XCD's L2) read over and over, by direct
+    global-to-LDS loads (to_lds) or loads into registers."""
+    lib = load()
+    dev = torch.device("cuda", torch.cuda.current_device())
+    src = torch.zeros(nbytes, device=dev, dtype=torch.uint8)
+    sink = torch.empty(blocks * 256, device=dev, dtype=torch.int32)
+    run = lambda: _check("ra_mb_l2_read", lib.ra_mb_l2_read(
+        src.data_ptr(), nbytes, int(to_lds), blocks, iters, sink.data_ptr(), _stream()))
+    run()
+    best = None
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        torch.cuda.synchronize()
+        gbs = blocks * iters * 65536 / (e0.elapsed_time(e1) * 1e6)
+        best = gbs if best is None else max(best, gbs)
+    return best

@@ -464,6 +464,11 @@ def test_microbench_exports_and_validation():
     assert lib.ra_mb_block_read(FAKE, 3 << 20, 4096, 4, FAKE, None) == 2   # not a power of two
     assert lib.ra_mb_block_read(FAKE, 8 * 4096, 4096, 4, FAKE, None) == 2  # under 16 blocks
     assert lib.ra_mb_block_read(FAKE, 1 << 20, 4096, 0, FAKE, None) == 2
+    assert lib.ra_mb_l2_read(None, 1 << 21, 1, 4, 10, FAKE, None) == 1
+    assert lib.ra_mb_l2_read(FAKE, 3 << 20, 1, 4, 10, FAKE, None) == 2    # not a power of two
+    assert lib.ra_mb_l2_read(FAKE, 1 << 15, 1, 4, 10, FAKE, None) == 2    # under 64 KiB
+    assert lib.ra_mb_l2_read(FAKE, 1 << 21, 0, 4, 0, FAKE, None) == 2     # no rounds
+    assert lib.ra_mb_l2_read(FAKE, 1 << 21, 0, 4, 1 << 25, FAKE, None) == 2
     assert lib.ra_mb_stream_read(FAKE, 4095, None, 4, FAKE, None) == 2
     assert lib.ra_mb_stream_read(None, 4096, None, 4, FAKE, None) == 1
     assert lib.ra_mb_mfma_bf16(None, 1, 1, FAKE, FAKE, None) == 1
